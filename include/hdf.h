@@ -1,0 +1,231 @@
+/*
+ * hdf.h -- C ABI of the HyperDFlash drafter-step library (libhdf.so), MI355X / gfx950.
+ *
+ * One decode round of HyperDFlash drafting (arxiv 2606.26744):
+ *   1. hdf_hc_reduce       gated residual reducer, Eq. (1) of Sec. 2.2
+ *   2. hdf_draft_block     one-pass DFlash block drafter over the reduced context
+ *                          (Sec. 1, Sec. 2.1; slot alignment of Sec. 2.3)
+ *   3. hdf_lm_head_argmax  draft logits z_k and greedy draft tokens (Sec. 2.3)
+ *   4. hdf_accept          greedy verification: longest agreeing prefix (Sec. 1, Sec. 3.4)
+ *
+ * Conventions shared by every call:
+ *   - Tensor arguments are DEVICE pointers unless marked "host".  Tensors are dense,
+ *     row-major, caller-allocated and caller-owned.  The library never allocates or
+ *     frees device memory; scratch space comes in through a caller-supplied workspace
+ *     whose size the matching *_workspace query returns.
+ *   - Calls are asynchronous: they validate, enqueue kernels on `stream` and return.
+ *     Outputs are valid once the stream has been synchronised.
+ *   - Errors are status codes; nothing throws across the ABI.  Argument errors are
+ *     detected on the host before anything is enqueued (HDF_E_INVALID,
+ *     HDF_E_UNSUPPORTED, HDF_E_WORKSPACE) and leave every output untouched.  A HIP
+ *     launch failure returns HDF_E_HIP.  hdf_last_error() describes the last failure
+ *     of the calling thread.
+ *   - Values that live in device memory (offsets, lengths, token ids) are
+ *     preconditions, not checked: offsets monotone, lengths within the stated
+ *     bounds, token ids in [0, vocab).
+ *   - Outputs never alias inputs.  Calls on different streams are independent;
+ *     the library keeps no state between calls.
+ *   - bf16 data is IEEE binary32 truncated to its upper 16 bits (1-8-7); conversions
+ *     to bf16 round to nearest, ties to even.  Inputs must be finite.
+ */
+#ifndef HDF_H_
+#define HDF_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* hdf_stream_t; /* a hipStream_t; NULL = the null stream */
+
+typedef enum {
+  HDF_OK = 0,
+  HDF_E_INVALID = 1,     /* null pointer, negative size, inconsistent shapes        */
+  HDF_E_UNSUPPORTED = 2, /* a valid request outside what the kernels implement      */
+  HDF_E_WORKSPACE = 3,   /* workspace missing or smaller than the *_workspace size  */
+  HDF_E_HIP = 4          /* a HIP runtime call or kernel launch failed               */
+} hdf_status;
+
+typedef enum { HDF_F32 = 0, HDF_BF16 = 1 } hdf_dtype;
+
+/* Text of the last failure on the calling thread ("" if none).  Valid until the
+ * thread's next hdf_* call. */
+const char* hdf_last_error(void);
+/* Library ABI version: major * 10000 + minor * 100 + patch. */
+int hdf_version(void);
+
+/* ------------------------------------------------------------------------------
+ * 1. Gated residual reducer -- Eq. (1), Sec. 2.2.
+ *
+ * For every token t of an m-path Hyper-Connection residual H_t (m rows of width d):
+ *     x      = vec(H_t)                         path-major: x[j*d + c] = H[t][j][c]
+ *     r      = 1 / sqrt(mean(x^2) + eps)        mean over all m*d entries
+ *     z_j    = gate_scale * r * (W_g[j] . x) + b_g[j]     (= W_g RMSNorm(x) + b)
+ *     alpha_j= sigmoid(z_j) + gate_offset       independent per-path gates
+ *     P_j    = H_t[j], or H_t[j] / sqrt(mean_c(H_t[j][c]^2) + eps) if per_path_norm
+ *     Y_t    = sum_j alpha_j P_j                summed in ascending j
+ * The paper's W_f (m x m*d) is W_g here, one contiguous row per gate.  gate_scale,
+ * gate_offset stand for the scale factor and small offset of the target's hc_head
+ * implementation (Sec. 2.2), which Eq. (1) abstracts away; per_path_norm is the
+ * drafter-side per-path RMSNorm Sec. 2.2 mentions.
+ *
+ * Arithmetic is fp32; Y is written in `dtype` (rounded once).
+ * ----------------------------------------------------------------------------*/
+typedef struct {
+  float eps;          /* RMSNorm epsilon (> 0); default 1e-6        */
+  float gate_scale;   /* default 1                                   */
+  float gate_offset;  /* default 0                                   */
+  int per_path_norm;  /* 0 (default) or 1                            */
+} hdf_reduce_params;
+
+/* H     [n_tok][m][d]  dtype
+ * W_g   [m][m*d]       dtype
+ * b_g   [m]            fp32
+ * params  host pointer or NULL for the defaults
+ * Y     [n_tok][d]     dtype (out)
+ * alpha [n_tok][m]     fp32 (out, may be NULL)
+ * Limits: 1 <= m <= 8; d % 8 == 0 (bf16) or d % 4 == 0 (fp32); d <= 8192 (bf16) or
+ * d <= 4096 (fp32); n_tok >= 0 (0 is a no-op).  Pointers 16-byte aligned. */
+hdf_status hdf_hc_reduce(const void* H, const void* W_g, const float* b_g, int64_t n_tok,
+                         int m, int d, hdf_dtype dtype, const hdf_reduce_params* params,
+                         void* Y, float* alpha, hdf_stream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * 2. One-pass block drafter (Sec. 1, Sec. 2.1, Sec. 2.3).
+ *
+ * Each sequence s has a context of T_s positions whose reduced states were
+ * produced by the reducer.  The drafter block holds B slots at positions
+ * T_s .. T_s+B-1: slot 0 is the accepted anchor token, slots 1..B-1 hold mask
+ * tokens (the anchor-plus-mask block input format, Sec. 2.1); slot k's final
+ * state predicts the token at position T_s + k (Sec. 2.3).
+ *
+ * Layer reading (the paper fixes the interface, not the layers): pre-norm
+ * transformer layers, multi-head attention with n_heads * head_dim = d, a
+ * SiLU-gated MLP of width d_ff, no biases, RMSNorms with fp32 weights.
+ *   context row i:  c = RMSNorm(y_i) * ctx_norm
+ *                   per layer K_i = RoPE(c Wk^T, pos i), V_i = c Wv^T   -> KV cache
+ *   block:          h = tok_emb[tokens]                      (fp32 residual stream)
+ *   per layer:      u = RMSNorm(h) * attn_norm
+ *                   Q,Kb,Vb = u Wq^T, u Wk^T, u Wv^T; RoPE on Q, Kb at T_s + k
+ *                   every block query attends to all T_s context keys and all B
+ *                   block keys, no mask (bidirectional in the block), softmax scale
+ *                   1/sqrt(head_dim)
+ *                   h += O Wo^T;  v = RMSNorm(h) * mlp_norm
+ *                   h += (SiLU(v Wgate^T) * (v Wup^T)) Wdown^T
+ *   output:         hidden = RMSNorm(h) * final_norm
+ * RoPE is rotate-half over the whole head: pair (i, i + head_dim/2) turns by
+ * pos * theta^(-2i/head_dim), with cos/sin taken from `rope_cs`.
+ * Stored intermediates (c, K, V, u, Q, attention output, v, SiLU*up, hidden) are
+ * rounded to `dtype`; h and all accumulations are fp32.
+ * ----------------------------------------------------------------------------*/
+typedef struct {
+  int n_layers, d, n_heads, head_dim, d_ff, vocab;
+  hdf_dtype dtype;
+  float eps;                     /* RMSNorm epsilon for every norm (> 0)                */
+  const void* tok_emb;           /* [vocab][d]                                          */
+  const float* ctx_norm;         /* [d] or NULL (all ones)                              */
+  const float* const* attn_norm; /* host array [n_layers] of device [d] (entries NULL = ones) */
+  const void* const* w_qkv;      /* host array [n_layers] of device [3d][d]: Wq;Wk;Wv rows */
+  const void* const* w_o;        /* host array [n_layers] of device [d][d]              */
+  const float* const* mlp_norm;  /* host array [n_layers] of device [d] (NULL = ones)   */
+  const void* const* w_gate_up;  /* host array [n_layers] of device [2*d_ff][d]: gate;up */
+  const void* const* w_down;     /* host array [n_layers] of device [d][d_ff]           */
+  const float* final_norm;       /* [d] or NULL                                         */
+  const float* rope_cs;          /* [rope_max_pos][head_dim/2][2] (cos, sin) fp32, or
+                                    NULL for no rotary embedding; see hdf_rope_table    */
+  int rope_max_pos;              /* positions 0 .. rope_max_pos-1 are tabulated         */
+} hdf_drafter;
+
+/* Fills a HOST buffer out[n_pos][head_dim/2][2] with cos and sin of
+ * pos * theta^(-2i/head_dim), evaluated in double precision and rounded to fp32.
+ * The caller copies it to the device once and passes it as hdf_drafter.rope_cs. */
+hdf_status hdf_rope_table(float* out_host, int n_pos, int head_dim, double theta);
+
+/* KV cache, caller-owned, `dtype` elements:
+ *   k  [n_layers][n_heads][kv_cap][head_dim]   keys after RoPE
+ *   vt [n_layers][n_heads][head_dim][kv_cap]   values, transposed (positions fastest)
+ * Context position i of sequence s lives at cache row kv_offsets[s] + i.  Every
+ * kv_offsets[s] must be a multiple of 64 and kv_offsets[s+1] - kv_offsets[s] >= T_s
+ * rounded up to a multiple of 64 (so 64-row tiles never leave a sequence's slot);
+ * kv_cap >= kv_offsets[n_seq].  Rows past T_s inside a slot are never used. */
+size_t hdf_kv_cache_bytes(const hdf_drafter* w, int64_t kv_cap); /* bytes of k (= of vt) */
+
+/* Workspace bytes hdf_draft_block needs for these sizes (0 on invalid arguments). */
+size_t hdf_draft_block_workspace(const hdf_drafter* w, int n_seq, int B, int64_t n_new,
+                                 int max_ctx);
+
+/* n_seq       sequences (0 is a no-op), B block slots (1..64)
+ * ctx_len     [n_seq] int32: T_s, the context length of sequence s (1..max_ctx)
+ * max_ctx     host: an upper bound on every T_s (sizes the attention grid)
+ * y_new       [n_new][d] dtype: reduced states of the context rows projected in this
+ *             call, packed by sequence
+ * new_offsets [n_seq+1] int32: rows new_offsets[s] .. new_offsets[s+1]-1 of y_new
+ *             belong to sequence s and are its LAST context positions
+ *             (T_s - n_s .. T_s - 1 with n_s = new_offsets[s+1] - new_offsets[s]);
+ *             new_offsets[0] = 0, new_offsets[n_seq] = n_new.  A cold step passes the
+ *             whole context (n_s = T_s); a warm step only the newest rows, the
+ *             earlier rows' keys/values being already in the cache.
+ * n_new       host: total new rows (>= 0)
+ * kv_offsets  [n_seq+1] int32: cache slot of each sequence (see above)
+ * kv_k, kv_vt, kv_cap  the KV cache; rows of the new positions are written
+ * tokens      [n_seq][B] int32: anchor then mask ids
+ * hidden      [n_seq*B][d] dtype (out): final-normed block states, row s*B + k
+ * ws, ws_bytes  workspace of at least hdf_draft_block_workspace(...) bytes, 256-byte
+ *             aligned; its contents on entry do not matter.
+ * Limits: head_dim in {64, 128}; n_heads * head_dim == d; d % 64 == 0;
+ *         d_ff % 64 == 0; max_ctx + B <= rope_max_pos when rope_cs is given. */
+hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t* ctx_len,
+                           int max_ctx, const void* y_new, const int32_t* new_offsets,
+                           int64_t n_new, const int32_t* kv_offsets, void* kv_k, void* kv_vt,
+                           int64_t kv_cap, const int32_t* tokens, void* hidden, void* ws,
+                           size_t ws_bytes, hdf_stream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * 3. LM head with fused greedy argmax (Sec. 2.3: z_k are the draft logits).
+ *
+ * logits[r][v] = sum_c hidden[r][c] * W_lm[v][c]   (fp32 accumulation)
+ * argmax[r]    = the smallest v with logits[r][v] == max_v logits[r][v]
+ * The full logits matrix is never stored unless `logits` is given.
+ * ----------------------------------------------------------------------------*/
+size_t hdf_lm_head_workspace(int64_t M, int vocab);
+
+/* hidden    [M][d] dtype; W_lm [vocab][d] dtype
+ * argmax    [M] int32 (out)
+ * max_logit [M] fp32 (out, may be NULL)
+ * logits    [M][vocab] fp32 (out, may be NULL; for tests)
+ * Limits: d % 64 == 0; 1 <= vocab < 2^31; M >= 0. */
+hdf_status hdf_lm_head_argmax(const void* hidden, const void* W_lm, int64_t M, int d, int vocab,
+                              hdf_dtype dtype, int32_t* argmax, float* max_logit, float* logits,
+                              void* ws, size_t ws_bytes, hdf_stream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * 4. Greedy acceptance (Sec. 1: the target keeps the longest draft prefix that
+ * agrees with its own tokens; Sec. 3.4: tau, the mean accepted length).
+ *
+ * For sequence s with drafts d_i = draft[s*draft_stride + i] (i = 0..K-1) and target
+ * tokens t_i = target[s*(K+1) + i] (i = 0..K):
+ *     n_s = max { j <= K : d_i == t_i for all i < j }
+ *     accept_len[s]  = n_s                 (tau of this round is n_s + 1)
+ *     next_anchor[s] = t_{n_s}             (the target's own next token)
+ *     commit_offsets = exclusive prefix sum of (n_s + 1), n_seq+1 entries
+ *     commit_tokens[commit_offsets[s] + i] = t_i for i = 0..n_s
+ * With the LM head's argmax array of a block (row s*B + k is slot k), the drafts
+ * are slots 1..B-1: draft = argmax + 1, draft_stride = B, K = B - 1.
+ * ----------------------------------------------------------------------------*/
+/* draft   int32, row s at draft + s*draft_stride, K entries (draft_stride >= K)
+ * target  [n_seq][K+1] int32
+ * accept_len, next_anchor  [n_seq] int32 (out)
+ * commit_offsets [n_seq+1] int32 (out, may be NULL)
+ * commit_tokens  [n_seq*(K+1)] int32 capacity (out, may be NULL)
+ * Limits: n_seq >= 0, 0 <= K <= 1024. */
+hdf_status hdf_accept(const int32_t* draft, int draft_stride, const int32_t* target, int n_seq,
+                      int K, int32_t* accept_len, int32_t* next_anchor, int32_t* commit_offsets,
+                      int32_t* commit_tokens, hdf_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HDF_H_ */

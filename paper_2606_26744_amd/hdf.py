@@ -1,0 +1,276 @@
+"""Python binding of libhdf (ctypes).  Argument marshalling only.
+
+Every computation runs in the HIP kernels of libhdf.so; this module turns torch
+tensors into device pointers, picks the current HIP stream, allocates output
+tensors with torch (device memory only) and raises on a non-OK status.  There is
+no fallback: if the library is missing, loading fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libhdf.so")
+
+HDF_F32, HDF_BF16 = 0, 1
+STATUS = {0: "HDF_OK", 1: "HDF_E_INVALID", 2: "HDF_E_UNSUPPORTED", 3: "HDF_E_WORKSPACE",
+          4: "HDF_E_HIP"}
+
+# Every symbol include/hdf.h declares.
+EXPORTS = ("hdf_last_error", "hdf_version", "hdf_hc_reduce", "hdf_rope_table",
+           "hdf_kv_cache_bytes", "hdf_draft_block_workspace", "hdf_draft_block",
+           "hdf_lm_head_workspace", "hdf_lm_head_argmax", "hdf_accept")
+
+
+class HdfError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class ReduceParams(ctypes.Structure):
+    _fields_ = [("eps", ctypes.c_float), ("gate_scale", ctypes.c_float),
+                ("gate_offset", ctypes.c_float), ("per_path_norm", ctypes.c_int)]
+
+
+class Drafter(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int), ("d", ctypes.c_int), ("n_heads", ctypes.c_int),
+                ("head_dim", ctypes.c_int), ("d_ff", ctypes.c_int), ("vocab", ctypes.c_int),
+                ("dtype", ctypes.c_int), ("eps", ctypes.c_float),
+                ("tok_emb", ctypes.c_void_p), ("ctx_norm", ctypes.c_void_p),
+                ("attn_norm", ctypes.POINTER(ctypes.c_void_p)),
+                ("w_qkv", ctypes.POINTER(ctypes.c_void_p)),
+                ("w_o", ctypes.POINTER(ctypes.c_void_p)),
+                ("mlp_norm", ctypes.POINTER(ctypes.c_void_p)),
+                ("w_gate_up", ctypes.POINTER(ctypes.c_void_p)),
+                ("w_down", ctypes.POINTER(ctypes.c_void_p)),
+                ("final_norm", ctypes.c_void_p), ("rope_cs", ctypes.c_void_p),
+                ("rope_max_pos", ctypes.c_int)]
+
+
+_lib = None
+_P, _I, _I64, _SZ, _F = (ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t,
+                         ctypes.c_float)
+
+
+def lib() -> ctypes.CDLL:
+    """Load libhdf.so (built in-tree by paper_2606_26744_amd.build)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python -m paper_2606_26744_amd.build` (no fallback exists)")
+    L = ctypes.CDLL(LIB_PATH)
+    L.hdf_last_error.restype = ctypes.c_char_p
+    L.hdf_last_error.argtypes = []
+    L.hdf_version.restype = _I
+    L.hdf_hc_reduce.restype = _I
+    L.hdf_hc_reduce.argtypes = [_P, _P, _P, _I64, _I, _I, _I, ctypes.POINTER(ReduceParams), _P, _P, _P]
+    L.hdf_rope_table.restype = _I
+    L.hdf_rope_table.argtypes = [_P, _I, _I, ctypes.c_double]
+    L.hdf_kv_cache_bytes.restype = _SZ
+    L.hdf_kv_cache_bytes.argtypes = [ctypes.POINTER(Drafter), _I64]
+    L.hdf_draft_block_workspace.restype = _SZ
+    L.hdf_draft_block_workspace.argtypes = [ctypes.POINTER(Drafter), _I, _I, _I64, _I]
+    L.hdf_draft_block.restype = _I
+    L.hdf_draft_block.argtypes = [ctypes.POINTER(Drafter), _I, _I, _P, _I, _P, _P, _I64, _P, _P, _P,
+                                  _I64, _P, _P, _P, _SZ, _P]
+    L.hdf_lm_head_workspace.restype = _SZ
+    L.hdf_lm_head_workspace.argtypes = [_I64, _I]
+    L.hdf_lm_head_argmax.restype = _I
+    L.hdf_lm_head_argmax.argtypes = [_P, _P, _I64, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]
+    L.hdf_accept.restype = _I
+    L.hdf_accept.argtypes = [_P, _I, _P, _I, _I, _P, _P, _P, _P, _P]
+    _lib = L
+    return L
+
+
+def _check(st: int):
+    if st != 0:
+        raise HdfError(st, lib().hdf_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return HDF_BF16
+    if t.dtype == torch.float32:
+        return HDF_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _dev(*ts):
+    for t in ts:
+        if t is not None:
+            if not t.is_cuda:
+                raise ValueError("libhdf takes device tensors")
+            if not t.is_contiguous():
+                raise ValueError("libhdf takes contiguous tensors")
+
+
+# ----------------------------------------------------------------------------- reducer
+
+def hc_reduce(H: torch.Tensor, W_g: torch.Tensor, b_g: torch.Tensor, *, eps: float = 1e-6,
+              gate_scale: float = 1.0, gate_offset: float = 0.0, per_path_norm: bool = False,
+              Y: Optional[torch.Tensor] = None, alpha: Optional[torch.Tensor] = None,
+              want_alpha: bool = False, stream=None):
+    """hdf_hc_reduce: H [n_tok, m, d], W_g [m, m*d], b_g [m] fp32 -> (Y [n_tok, d], alpha)."""
+    n, m, d = H.shape
+    if Y is None:
+        Y = torch.empty((n, d), dtype=H.dtype, device=H.device)
+    if alpha is None and want_alpha:
+        alpha = torch.empty((n, m), dtype=torch.float32, device=H.device)
+    _dev(H, W_g, b_g, Y, alpha)
+    p = ReduceParams(eps, gate_scale, gate_offset, int(per_path_norm))
+    _check(lib().hdf_hc_reduce(_ptr(H), _ptr(W_g), _ptr(b_g), n, m, d, _dt(H), ctypes.byref(p),
+                               _ptr(Y), _ptr(alpha), _stream(stream)))
+    return Y, alpha
+
+
+# ----------------------------------------------------------------------------- accept
+
+def accept(draft: torch.Tensor, target: torch.Tensor, *, K: Optional[int] = None,
+           draft_stride: Optional[int] = None, commits: bool = True, stream=None):
+    """hdf_accept.  draft: int32 with row s at s*draft_stride (a [n_seq, >=K] tensor or a
+    view into a bigger array), target [n_seq, K+1] int32."""
+    n_seq = target.shape[0]
+    K = target.shape[1] - 1 if K is None else K
+    if draft_stride is None:
+        draft_stride = draft.stride(0) if draft.dim() == 2 else K
+    dev = target.device
+    acc = torch.empty(n_seq, dtype=torch.int32, device=dev)
+    anc = torch.empty(n_seq, dtype=torch.int32, device=dev)
+    offs = torch.empty(n_seq + 1, dtype=torch.int32, device=dev) if commits else None
+    toks = torch.empty(max(1, n_seq * (K + 1)), dtype=torch.int32, device=dev) if commits else None
+    _dev(target, acc)
+    if not draft.is_cuda:
+        raise ValueError("libhdf takes device tensors")
+    _check(lib().hdf_accept(_ptr(draft), draft_stride, _ptr(target), n_seq, K, _ptr(acc),
+                            _ptr(anc), _ptr(offs), _ptr(toks), _stream(stream)))
+    return acc, anc, offs, toks
+
+
+# ----------------------------------------------------------------------------- LM head
+
+def lm_head_workspace(M: int, vocab: int) -> int:
+    return int(lib().hdf_lm_head_workspace(M, vocab))
+
+
+def lm_head_argmax(hidden: torch.Tensor, w_lm: torch.Tensor, *, want_logits: bool = False,
+                   want_max: bool = True, ws: Optional[torch.Tensor] = None, out=None,
+                   stream=None):
+    """hdf_lm_head_argmax: hidden [M, d], w_lm [V, d] -> (argmax int32 [M], max fp32 [M],
+    logits fp32 [M, V] or None)."""
+    M, d = hidden.shape
+    V = w_lm.shape[0]
+    dev = hidden.device
+    if out is None:
+        am = torch.empty(M, dtype=torch.int32, device=dev)
+        mx = torch.empty(M, dtype=torch.float32, device=dev) if want_max else None
+    else:
+        am, mx = out
+    lg = torch.empty((M, V), dtype=torch.float32, device=dev) if want_logits else None
+    need = lm_head_workspace(M, V)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _dev(hidden, w_lm, am, mx, lg, ws)
+    _check(lib().hdf_lm_head_argmax(_ptr(hidden), _ptr(w_lm), M, d, V, _dt(hidden), _ptr(am),
+                                    _ptr(mx), _ptr(lg), _ptr(ws), ws.numel(), _stream(stream)))
+    return am, mx, lg
+
+
+# ----------------------------------------------------------------------------- drafter
+
+def rope_table(n_pos: int, head_dim: int, theta: float) -> torch.Tensor:
+    """Host-computed (fp64 -> fp32) cos/sin table [n_pos, head_dim/2, 2] on the CPU."""
+    t = torch.empty((n_pos, head_dim // 2, 2), dtype=torch.float32)
+    _check(lib().hdf_rope_table(ctypes.c_void_p(t.data_ptr()), n_pos, head_dim, theta))
+    return t
+
+
+class DrafterHandle:
+    """Keeps the device weights and the ctypes hdf_drafter struct alive together."""
+
+    def __init__(self, weights: dict, *, n_layers: int, d: int, n_heads: int, head_dim: int,
+                 d_ff: int, vocab: int, eps: float = 1e-6, rope_theta: float = 10000.0,
+                 rope_max_pos: int = 0, device="cuda"):
+        self.w = weights
+        self.L = n_layers
+        dt = weights["tok_emb"].dtype
+        self.torch_dtype = dt
+        keep = []
+
+        def arr(ts):
+            a = (ctypes.c_void_p * n_layers)(*[None if t is None else t.data_ptr() for t in ts])
+            keep.append(a)
+            return ctypes.cast(a, ctypes.POINTER(ctypes.c_void_p))
+
+        self.rope = None
+        if rope_theta and rope_theta > 0:
+            self.rope = rope_table(rope_max_pos, head_dim, rope_theta).to(device)
+        self.s = Drafter(
+            n_layers, d, n_heads, head_dim, d_ff, vocab, _dt(weights["tok_emb"]), eps,
+            weights["tok_emb"].data_ptr(),
+            None if weights.get("ctx_norm") is None else weights["ctx_norm"].data_ptr(),
+            arr(weights.get("attn_norm", [None] * n_layers)), arr(weights["w_qkv"]),
+            arr(weights["w_o"]), arr(weights.get("mlp_norm", [None] * n_layers)),
+            arr(weights["w_gate_up"]), arr(weights["w_down"]),
+            None if weights.get("final_norm") is None else weights["final_norm"].data_ptr(),
+            None if self.rope is None else self.rope.data_ptr(),
+            rope_max_pos if self.rope is not None else 0)
+        self._keep = keep
+        self.d, self.nh, self.hd, self.F, self.V = d, n_heads, head_dim, d_ff, vocab
+
+    def kv_cache_bytes(self, kv_cap: int) -> int:
+        return int(lib().hdf_kv_cache_bytes(ctypes.byref(self.s), kv_cap))
+
+    def workspace_bytes(self, n_seq: int, B: int, n_new: int, max_ctx: int) -> int:
+        return int(lib().hdf_draft_block_workspace(ctypes.byref(self.s), n_seq, B, n_new, max_ctx))
+
+    def alloc_kv(self, kv_cap: int, device="cuda"):
+        shape_k = (self.L, self.nh, kv_cap, self.hd)
+        shape_vt = (self.L, self.nh, self.hd, kv_cap)
+        return (torch.zeros(shape_k, dtype=self.torch_dtype, device=device),
+                torch.zeros(shape_vt, dtype=self.torch_dtype, device=device))
+
+    def draft_block(self, *, ctx_len: torch.Tensor, max_ctx: int, y_new: torch.Tensor,
+                    new_offsets: torch.Tensor, kv_offsets: torch.Tensor, kv_k: torch.Tensor,
+                    kv_vt: torch.Tensor, tokens: torch.Tensor, hidden: Optional[torch.Tensor] = None,
+                    ws: Optional[torch.Tensor] = None, stream=None):
+        n_seq, B = tokens.shape
+        n_new = y_new.shape[0]
+        kv_cap = kv_k.shape[2]
+        dev = tokens.device
+        if hidden is None:
+            hidden = torch.empty((n_seq * B, self.d), dtype=self.torch_dtype, device=dev)
+        need = self.workspace_bytes(n_seq, B, n_new, max_ctx)
+        if ws is None or ws.numel() < need:
+            ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        _dev(ctx_len, y_new, new_offsets, kv_offsets, kv_k, kv_vt, tokens, hidden, ws)
+        _check(lib().hdf_draft_block(ctypes.byref(self.s), n_seq, B, _ptr(ctx_len), max_ctx,
+                                     _ptr(y_new), _ptr(new_offsets), n_new, _ptr(kv_offsets),
+                                     _ptr(kv_k), _ptr(kv_vt), kv_cap, _ptr(tokens), _ptr(hidden),
+                                     _ptr(ws), ws.numel(), _stream(stream)))
+        return hidden
+
+
+def kv_slot_offsets(ctx_lens: Sequence[int]) -> list:
+    """Cache slot offsets: each sequence's slot starts at a multiple of 64 rows and holds
+    its context length rounded up to 64."""
+    offs = [0]
+    for t in ctx_lens:
+        offs.append(offs[-1] + ((int(t) + 63) // 64) * 64)
+    return offs

@@ -1,0 +1,55 @@
+"""Parity tolerances, stated once.
+
+fp32 outputs: per row, max|gpu - ref| <= 1e-4 * max|ref| (relative to the row's
+scale; elementwise relative error is meaningless near zero).
+bf16 outputs: |gpu - ref| <= max(2e-2, one bf16 ulp of ref) elementwise.  Both
+sides round the same exact quantity to bf16; a float32-vs-float64 difference far
+below one ulp can still land on opposite sides of a rounding boundary, which
+moves the stored value by exactly one ulp, so one ulp is allowed even where it
+exceeds 2e-2 (|ref| >= 4).
+"""
+import numpy as np
+
+
+def bf16_ulp(x):
+    a = np.abs(np.asarray(x, dtype=np.float64))
+    a = np.maximum(a, 2.0 ** -126)
+    return 2.0 ** (np.floor(np.log2(a)) - 7)
+
+
+def assert_bf16_close(got, ref, what=""):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    tol = np.maximum(2e-2, bf16_ulp(ref))
+    err = np.abs(got - ref)
+    bad = err > tol
+    if bad.any():
+        i = np.argwhere(bad)[0]
+        raise AssertionError(f"{what}: {int(bad.sum())} of {bad.size} outside tolerance; first at "
+                             f"{tuple(i)}: got {got[tuple(i)]!r} ref {ref[tuple(i)]!r}")
+    return int(np.count_nonzero(got != ref))
+
+
+def assert_f32_rows_close(got, ref, what="", rel=1e-4):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    g2 = got.reshape(got.shape[0], -1) if got.ndim > 1 else got[:, None]
+    r2 = ref.reshape(ref.shape[0], -1) if ref.ndim > 1 else ref[:, None]
+    scale = np.maximum(np.abs(r2).max(axis=1), 1e-30)
+    err = np.abs(g2 - r2).max(axis=1)
+    bad = err > rel * scale
+    if bad.any():
+        i = int(np.argmax(bad))
+        raise AssertionError(f"{what}: {int(bad.sum())} rows outside {rel} relative; row {i}: "
+                             f"max err {err[i]!r} vs scale {scale[i]!r}")
+
+
+def assert_abs_close(got, ref, atol, what=""):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    err = np.abs(got - ref)
+    if (err > atol).any():
+        i = np.unravel_index(int(np.argmax(err)), err.shape)
+        raise AssertionError(f"{what}: max abs err {err[i]!r} at {i} > {atol}")

@@ -1,0 +1,86 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports every
+symbol include/hdf.h declares, and rejects bad arguments before touching a device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_26744_amd import hdf
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_symbols():
+    src = open(os.path.join(ROOT, "include", "hdf.h")).read()
+    return sorted(set(re.findall(r"\b(hdf_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = hdf.lib()
+    declared = _declared_symbols()
+    assert declared, "no declarations found"
+    for name in declared:
+        assert hasattr(L, name), name
+    assert sorted(hdf.EXPORTS) == declared
+    assert L.hdf_version() >= 100
+
+
+def _status(st):
+    return hdf.STATUS[st]
+
+
+def test_reduce_validation():
+    L = hdf.lib()
+    P = ctypes.c_void_p
+    fake = P(4096)   # never dereferenced: every call below fails validation first
+    bad = [
+        dict(n=-1, m=4, d=64, dt=1),
+        dict(n=1, m=0, d=64, dt=1),
+        dict(n=1, m=9, d=64, dt=1),
+        dict(n=1, m=4, d=60, dt=1),       # bf16 needs d % 8 == 0
+        dict(n=1, m=4, d=6, dt=0),        # fp32 needs d % 4 == 0
+        dict(n=1, m=4, d=64, dt=7),
+    ]
+    for b in bad:
+        st = L.hdf_hc_reduce(fake, fake, fake, b["n"], b["m"], b["d"], b["dt"], None, fake, None, None)
+        assert _status(st) == "HDF_E_INVALID", b
+    st = L.hdf_hc_reduce(fake, fake, fake, 1, 4, 8200, 1, None, fake, None, None)
+    assert _status(st) == "HDF_E_UNSUPPORTED"
+    st = L.hdf_hc_reduce(None, fake, fake, 1, 4, 64, 1, None, fake, None, None)
+    assert _status(st) == "HDF_E_INVALID"
+    assert b"null" in L.hdf_last_error()
+    p = hdf.ReduceParams(0.0, 1.0, 0.0, 0)
+    st = L.hdf_hc_reduce(fake, fake, fake, 1, 4, 64, 1, ctypes.byref(p), fake, None, None)
+    assert _status(st) == "HDF_E_INVALID"
+    # misaligned pointers
+    st = L.hdf_hc_reduce(P(4098), fake, fake, 1, 4, 64, 1, None, fake, None, None)
+    assert _status(st) == "HDF_E_INVALID"
+    # n_tok = 0 is a no-op that succeeds without touching anything
+    st = L.hdf_hc_reduce(None, None, None, 0, 4, 64, 1, None, None, None, None)
+    assert _status(st) == "HDF_OK" and L.hdf_last_error() == b""
+
+
+def test_accept_validation():
+    L = hdf.lib()
+    fake = ctypes.c_void_p(4096)
+    assert _status(L.hdf_accept(fake, 15, fake, -1, 15, fake, fake, None, None, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_accept(fake, 15, fake, 1, 1025, fake, fake, None, None, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_accept(fake, 3, fake, 1, 15, fake, fake, None, None, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_accept(fake, 15, None, 1, 15, fake, fake, None, None, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_accept(None, 15, None, 0, 15, None, None, None, None, None)) == "HDF_OK"
+
+
+def test_rope_table_host_values():
+    import math
+    t = hdf.rope_table(5, 8, 10000.0)
+    for p in range(5):
+        for i in range(4):
+            a = p * 10000.0 ** (-2.0 * i / 8)
+            assert t[p, i, 0].item() == pytest.approx(math.cos(a), abs=1e-7)
+            assert t[p, i, 1].item() == pytest.approx(math.sin(a), abs=1e-7)
+    L = hdf.lib()
+    assert _status(L.hdf_rope_table(None, 4, 8, 1e4)) == "HDF_E_INVALID"
+    buf = (ctypes.c_float * 64)()
+    assert _status(L.hdf_rope_table(buf, 4, 7, 1e4)) == "HDF_E_INVALID"
+    assert _status(L.hdf_rope_table(buf, 4, 8, 0.0)) == "HDF_E_INVALID"
