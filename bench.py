@@ -1,0 +1,228 @@
+#!/usr/bin/env python3
+"""Benchmark of one HyperDFlash drafter step on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input:
+    gated reduce of the newest context rows -> block draft (context K/V append,
+    attention over cached context + block, MLP) -> LM head argmax -> acceptance.
+Workload (default): the full-size warm step -- 8 sequences with 2048 context
+positions each, 16 of them new this round (reduced and projected), a drafter of
+d=4096 (32 heads x 128, SiLU MLP 12288), vocabulary 129280, block B=16; bf16 storage
+with fp32 accumulation; seeded synthetic weights and inputs already resident in HBM.
+
+Prints ONE JSON line (rank 0 of a single process).  Extras: per-stage times, the LM
+head's roofline (the dominant kernel, timed live with HIP events on the stream it runs
+on), the reducer at its bandwidth-stress size, and the CPU oracle timed on a bounded
+sample on this host.
+"""
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+METRIC = "draft blocks/sec at d=4096,B=16,V=129280; reducer HBM GB/s; MFMA util %"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-reducer-stress", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run a plain 2 GiB device copy (counter calibration)")
+    return ap.parse_args()
+
+
+def build_workload(torch, synth, hdf):
+    from paper_2606_26744_amd.step import StepBuffers
+    wl = synth.drafter_full()
+    dr = wl.drafter
+    n_seq, T, B, n_s = wl.n_seq, wl.ctx_lens[0], wl.block, wl.new_rows
+    dev = "cuda"
+    w = synth.drafter_weights(wl, device=dev)
+    h = hdf.DrafterHandle(w, n_layers=dr.n_layers, d=dr.d, n_heads=dr.n_heads,
+                          head_dim=dr.head_dim, d_ff=dr.d_ff, vocab=dr.vocab, eps=dr.eps,
+                          rope_theta=dr.rope_theta, rope_max_pos=T + B)
+    offs = hdf.kv_slot_offsets([T] * n_seq)
+    kv_k, kv_vt = h.alloc_kv(offs[-1])
+    nh, hd = dr.n_heads, dr.head_dim
+    t0 = T - n_s
+    for s in range(n_seq):          # rows of earlier rounds, already in the cache
+        for l in range(dr.n_layers):
+            k, v = synth.kv_prefix(wl, t0, l, device=dev, sub=s)
+            o = offs[s]
+            kv_k[l, :, o:o + t0, :] = k.view(t0, nh, hd).permute(1, 0, 2)
+            kv_vt[l, :, :, o:o + t0] = v.view(t0, nh, hd).permute(1, 2, 0)
+    red = synth.reducer_inputs(wl, n_seq * n_s, device=dev)
+    i32 = dict(dtype=torch.int32, device=dev)
+    args = dict(H_new=red["H"], W_g=red["W_g"], b_g=red["b_g"],
+                new_offsets=torch.arange(0, n_seq * n_s + 1, n_s, **i32),
+                ctx_len=torch.full((n_seq,), T, **i32), max_ctx=T,
+                kv_offsets=torch.tensor(offs, **i32), kv_k=kv_k, kv_vt=kv_vt,
+                tokens=synth.block_tokens(wl, device=dev))
+    bufs = StepBuffers(h, n_seq, B, n_seq * n_s, T, wl.m)
+    return wl, h, bufs, args, red, w, offs
+
+
+def cpu_baseline(torch, synth, wl, h, w, red, args, offs):
+    """The oracle as it stands, on one of the eight sequences of the same step."""
+    import numpy as np
+    from oracle.accept import accept
+    from oracle.drafter import Weights, draft_block
+    from oracle.lm_head import lm_head_argmax
+    from oracle.reducer import hc_reduce
+    dr = wl.drafter
+    b = synth.to_numpy_bits
+    n_s, T, B = wl.new_rows, wl.ctx_lens[0], wl.block
+    t0 = T - n_s
+    s = 0
+    wb = {k: ([b(x) for x in v] if isinstance(v, list) else b(v)) for k, v in w.items()}
+    W = Weights(wb, d=dr.d, n_layers=dr.n_layers, n_heads=dr.n_heads, head_dim=dr.head_dim,
+                d_ff=dr.d_ff, vocab=dr.vocab, eps=dr.eps, rope_theta=dr.rope_theta, dtype="bf16")
+    pre = []
+    nh, hd = dr.n_heads, dr.head_dim
+    for l in range(dr.n_layers):
+        k = args["kv_k"][l, :, offs[s]:offs[s] + t0, :].permute(1, 0, 2).reshape(t0, -1)
+        v = args["kv_vt"][l, :, :, offs[s]:offs[s] + t0].permute(2, 0, 1).reshape(t0, -1)
+        pre.append((b(k.contiguous()), b(v.contiguous())))
+    H = b(red["H"][:n_s])
+    Wg, bg = b(red["W_g"]), b(red["b_g"])
+    toks = b(args["tokens"])[:1]
+    times = []
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    for rep in range(2):
+        t_start = time.perf_counter()
+        y, _ = hc_reduce(H, Wg, bg, dtype="bf16")
+        hid = draft_block(W, [y], toks, kv_prefix=[pre])
+        am, _, _ = lm_head_argmax(hid, W.w_lm)
+        drafts = am[1:][None]
+        tg = synth.make_targets(drafts, [0.8], dr.vocab, seed=wl.seed)
+        accept(drafts, tg)
+        times.append(time.perf_counter() - t_start)
+    t = min(times)
+    cpu = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": round(1.0 / t, 4), "unit": "blocks/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"1 of {wl.n_seq} sequences of the same warm step (16 new context rows "
+                      f"reduced and projected, 2048-position context, B=16, full vocabulary "
+                      f"argmax); best of {len(times)} runs, {t:.2f} s each; float64 NumPy; "
+                      f"host CPU {cpu}; affinity {len(os.sched_getaffinity(0))} cores"}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {a.gpus}); the drafter step "
+              f"shards by sequence with no exchange, so run one process per GPU.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import synth
+    from paper_2606_26744_amd import hdf
+    from paper_2606_26744_amd.step import drafter_step
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    hdf.lib()
+    wl, h, bufs, args, red, w, offs = build_workload(torch, synth, hdf)
+    n_seq, B = wl.n_seq, wl.block
+    # Targets: copies of the drafts with probability 0.8 per position (drafts from one
+    # untimed step), so acceptance lengths are geometric as in the workload description.
+    out = drafter_step(h, bufs, targets=None, **args)
+    torch.cuda.synchronize()
+    drafts = out["argmax"].view(n_seq, B)[:, 1:].cpu().numpy()
+    tg = torch.as_tensor(synth.make_targets(drafts, wl.match_p, wl.drafter.vocab,
+                                            seed=wl.seed)).cuda()
+    for _ in range(a.warmup):
+        drafter_step(h, bufs, targets=tg, **args)
+    torch.cuda.synchronize()
+    marks = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(a.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for i in range(a.steps):
+        out = drafter_step(h, bufs, targets=tg, marks=marks[i], **args)
+    t_end.record()
+    torch.cuda.synchronize()
+    ms = t_start.elapsed_time(t_end) / a.steps
+    names = ["reduce", "draft_block", "lm_head_argmax", "accept"]
+    stage_us = {n: statistics.mean(m[j].elapsed_time(m[j + 1]) * 1e3 for m in marks)
+                for j, n in enumerate(names)}
+    acc = out["accept_len"].cpu().numpy()
+    # LM head roofline: algorithmic bytes of one launch (weights + hidden + outputs).
+    d, V, M = wl.d, wl.drafter.vocab, n_seq * B
+    lm_bytes = V * d * 2 + M * d * 2 + M * 8
+    lm_us = stage_us["lm_head_argmax"]
+    lm_gbs = lm_bytes / (lm_us * 1e-6) / 1e9
+    lm_tflops = 2.0 * M * d * V / (lm_us * 1e-6) / 1e12
+    res = {
+        "metric": METRIC, "value": round(n_seq / (ms * 1e-3), 1), "unit": "blocks/s",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded; random-init weights of the drafter shape)",
+        "config": {"workload": "drafter_full_warm", "n_seq": n_seq, "context": wl.ctx_lens[0],
+                   "new_rows_per_seq": wl.new_rows, "d": d, "heads": wl.drafter.n_heads,
+                   "head_dim": wl.drafter.head_dim, "d_ff": wl.drafter.d_ff, "vocab": V,
+                   "block": B, "m_paths": wl.m, "layers": wl.drafter.n_layers,
+                   "parallelism": "single GPU"},
+        "stages_us": {k: round(v, 2) for k, v in stage_us.items()},
+        "roofline": {"kernel": "lm_head_argmax", "bound": "hbm", "achieved": round(lm_gbs, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(lm_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": None, "bytes_per_launch": lm_bytes,
+                     "mfma_tflops": round(lm_tflops, 1),
+                     "mfma_frac": round(lm_tflops / BF16_PEAK_TFLOPS, 4)},
+        "mean_accept_len": float(acc.mean()), "tau": float(acc.mean() + 1),
+    }
+    if not a.no_reducer_stress:
+        sw = synth.reducer_stress()
+        ri = synth.reducer_inputs(sw, sw.n_tok, device="cuda")
+        Y = torch.empty((sw.n_tok, sw.d), dtype=torch.bfloat16, device="cuda")
+        for _ in range(3):
+            hdf.hc_reduce(ri["H"], ri["W_g"], ri["b_g"], Y=Y)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        n_it = 20
+        for _ in range(n_it):
+            hdf.hc_reduce(ri["H"], ri["W_g"], ri["b_g"], Y=Y)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / n_it * 1e3
+        rb = sw.n_tok * sw.m * sw.d * 2 + sw.n_tok * sw.d * 2 + sw.m * sw.m * sw.d * 2
+        res["reducer_stress"] = {"n_tok": sw.n_tok, "m": sw.m, "d": sw.d, "us": round(us, 1),
+                                 "GB/s": round(rb / (us * 1e-6) / 1e9, 1),
+                                 "frac_hbm": round(rb / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                                 "bytes_per_launch": rb}
+        del ri, Y
+        torch.cuda.empty_cache()
+    if a.copy_probe:
+        x = torch.empty(1 << 31, dtype=torch.uint8, device="cuda")
+        y = torch.empty_like(x)
+        for _ in range(5):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        del x, y
+    if not a.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(torch, synth, wl, h, w, red, args, offs)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

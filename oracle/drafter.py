@@ -77,12 +77,12 @@ class Weights:
         self.d, self.L, self.nh, self.hd = d, n_layers, n_heads, head_dim
         self.F, self.V, self.eps, self.theta, self.dtype = d_ff, vocab, eps, rope_theta, dtype
         assert n_heads * head_dim == d
-        self.tok_emb = as_f64(w["tok_emb"])
+        self.tok_emb = w["tok_emb"]          # decoded row by row on use
         self.w_qkv = [as_f64(x) for x in w["w_qkv"]]
         self.w_o = [as_f64(x) for x in w["w_o"]]
         self.w_gate_up = [as_f64(x) for x in w["w_gate_up"]]
         self.w_down = [as_f64(x) for x in w["w_down"]]
-        self.w_lm = as_f64(w["w_lm"]) if w.get("w_lm") is not None else None
+        self.w_lm = w.get("w_lm")            # decoded by the LM head
 
         def g(x):
             return None if x is None else np.asarray(x, dtype=np.float64)
@@ -124,7 +124,7 @@ def block_forward(W: Weights, ctx_kv: Sequence[Tuple[np.ndarray, np.ndarray]],
     T = ctx_kv[0][0].shape[0]
     B = len(tokens)
     pos = pos_shift + T + np.arange(B)
-    h = round_f32(W.tok_emb[np.asarray(tokens, dtype=np.int64)])   # fp32 residual stream
+    h = round_f32(as_f64(np.asarray(W.tok_emb)[np.asarray(tokens, dtype=np.int64)]))  # fp32 residual
     for l in range(W.L):
         u = store(rmsnorm(h, W.attn_norm[l], W.eps), dt)
         qkv = u @ W.w_qkv[l].T

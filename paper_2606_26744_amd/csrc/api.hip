@@ -54,6 +54,95 @@ int device_cu_count() {
 
 }  // namespace hdf
 
+
+// ---------------------------------------------------------------- drafter planning
+namespace {
+
+constexpr int64_t kCtxChunk = 16384;  // context rows projected per GEMM launch
+
+hdf_status validate_drafter(const hdf_drafter* w) {
+  if (w == nullptr) return fail(HDF_E_INVALID, "drafter: null");
+  if (w->dtype != HDF_F32 && w->dtype != HDF_BF16) return fail(HDF_E_INVALID, "drafter: bad dtype");
+  if (w->n_layers < 1) return fail(HDF_E_INVALID, "drafter: n_layers < 1");
+  if (w->d <= 0 || w->n_heads <= 0 || w->head_dim <= 0 || w->d_ff <= 0 || w->vocab <= 0)
+    return fail(HDF_E_INVALID, "drafter: non-positive size");
+  if (int64_t(w->n_heads) * w->head_dim != w->d)
+    return fail(HDF_E_INVALID, "drafter: n_heads * head_dim != d");
+  if (w->head_dim != 64 && w->head_dim != 128)
+    return fail(HDF_E_UNSUPPORTED, "drafter: head_dim %d not in {64, 128}", w->head_dim);
+  if (w->d % 64 != 0 || w->d > 8192)
+    return fail(HDF_E_UNSUPPORTED, "drafter: d=%d must be a multiple of 64 up to 8192", w->d);
+  if (w->d_ff % 64 != 0) return fail(HDF_E_UNSUPPORTED, "drafter: d_ff %% 64 != 0");
+  if (!(w->eps > 0.f)) return fail(HDF_E_INVALID, "drafter: eps must be > 0");
+  if (w->tok_emb == nullptr || w->w_qkv == nullptr || w->w_o == nullptr ||
+      w->w_gate_up == nullptr || w->w_down == nullptr || w->attn_norm == nullptr ||
+      w->mlp_norm == nullptr)
+    return fail(HDF_E_INVALID, "drafter: null weight pointer");
+  for (int l = 0; l < w->n_layers; ++l)
+    if (w->w_qkv[l] == nullptr || w->w_o[l] == nullptr || w->w_gate_up[l] == nullptr ||
+        w->w_down[l] == nullptr)
+      return fail(HDF_E_INVALID, "drafter: null weight of layer %d", l);
+  if (w->rope_cs != nullptr && w->rope_max_pos < 1)
+    return fail(HDF_E_INVALID, "drafter: rope_max_pos < 1 with a RoPE table");
+  return HDF_OK;
+}
+
+struct DraftPlan {
+  size_t plan_pos, plan_row, c, h, u, q, kb, vtb, parts, part_o, part_ml, attn, act, total;
+  int chunk_len;
+};
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+DraftPlan plan_workspace(const hdf_drafter& w, int n_seq, int B, int64_t n_new, int max_ctx) {
+  DraftPlan P{};
+  const bool bf = w.dtype == HDF_BF16;
+  const size_t el = bf ? 2 : 4;
+  const size_t d = w.d, F = w.d_ff;
+  const size_t M = size_t(n_seq) * B;
+  const size_t QB = size_t((B + 15) / 16) * 16;
+  const int64_t crow = n_new < kCtxChunk ? n_new : kCtxChunk;
+  P.chunk_len = 512;
+  const size_t n_chunks = size_t((max_ctx + P.chunk_len - 1) / P.chunk_len);
+  size_t parts = 0;
+  auto upd = [&](int64_t rows, int N, int K) {
+    if (rows <= 0) return;
+    const size_t sp = size_t(hdf::gemm_pick_splits(bf, int(rows), N, K));
+    const size_t b = sp * size_t(rows) * size_t(N) * 4;
+    if (b > parts) parts = b;
+  };
+  upd(crow, 2 * w.d, w.d);
+  upd(n_new % kCtxChunk, 2 * w.d, w.d);  // a shorter last chunk may split further
+  upd(int64_t(M), 3 * w.d, w.d);
+  upd(int64_t(M), w.d, w.d);
+  upd(int64_t(M), 2 * w.d_ff, w.d);
+  upd(int64_t(M), w.d, w.d_ff);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align256(bytes);
+    return o;
+  };
+  P.plan_pos = take(size_t(n_new) * 4);
+  P.plan_row = take(size_t(n_new) * 4);
+  P.c = take(size_t(crow) * d * el);
+  P.h = take(M * d * 4);
+  P.u = take(M * d * el);
+  P.q = take(M * d * el);
+  P.kb = take(size_t(w.n_heads) * size_t(n_seq) * 64 * w.head_dim * el);
+  P.vtb = take(size_t(w.n_heads) * size_t(n_seq) * 64 * w.head_dim * el);
+  P.parts = take(parts);
+  const size_t pslots = size_t(n_seq) * w.n_heads * (n_chunks + 1) * QB;
+  P.part_o = take(pslots * w.head_dim * 4);
+  P.part_ml = take(pslots * 2 * 4);
+  P.attn = take(M * d * el);
+  P.act = take(M * F * el);
+  P.total = off;
+  return P;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* hdf_last_error(void) { return g_err; }
@@ -135,8 +224,9 @@ size_t hdf_kv_cache_bytes(const hdf_drafter* w, int64_t kv_cap) {
 
 size_t hdf_draft_block_workspace(const hdf_drafter* w, int n_seq, int B, int64_t n_new,
                                  int max_ctx) {
-  (void)w; (void)n_seq; (void)B; (void)n_new; (void)max_ctx;
-  return 0;
+  if (validate_drafter(w) != HDF_OK || n_seq < 0 || B < 1 || B > 64 || n_new < 0 || max_ctx < 0)
+    return 0;
+  return plan_workspace(*w, n_seq, B, n_new, max_ctx).total;
 }
 
 hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t* ctx_len,
@@ -144,15 +234,160 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
                            int64_t n_new, const int32_t* kv_offsets, void* kv_k, void* kv_vt,
                            int64_t kv_cap, const int32_t* tokens, void* hidden, void* ws,
                            size_t ws_bytes, hdf_stream_t stream) {
-  return fail(HDF_E_UNSUPPORTED, "draft_block: not built yet");
+  hdf_status st = validate_drafter(w);
+  if (st != HDF_OK) return st;
+  if (n_seq < 0) return fail(HDF_E_INVALID, "draft_block: n_seq < 0");
+  if (B < 1 || B > 64) return fail(HDF_E_INVALID, "draft_block: B=%d outside [1, 64]", B);
+  if (max_ctx < 0 || n_new < 0) return fail(HDF_E_INVALID, "draft_block: negative size");
+  if (kv_cap < 0 || kv_cap % 64 != 0)
+    return fail(HDF_E_INVALID, "draft_block: kv_cap must be a non-negative multiple of 64");
+  if (w->rope_cs != nullptr && int64_t(max_ctx) + B > w->rope_max_pos)
+    return fail(HDF_E_INVALID, "draft_block: max_ctx + B exceeds the RoPE table (%d)",
+                w->rope_max_pos);
+  if (n_seq == 0) return ok();
+  if (ctx_len == nullptr || kv_offsets == nullptr || tokens == nullptr || hidden == nullptr)
+    return fail(HDF_E_INVALID, "draft_block: null pointer");
+  if (n_new > 0 && (y_new == nullptr || new_offsets == nullptr))
+    return fail(HDF_E_INVALID, "draft_block: null y_new/new_offsets with n_new > 0");
+  if ((n_new > 0 || max_ctx > 0) && (kv_k == nullptr || kv_vt == nullptr || kv_cap == 0))
+    return fail(HDF_E_INVALID, "draft_block: a context needs a KV cache");
+  if (!aligned16(hidden) || (y_new && !aligned16(y_new)) || (kv_k && !aligned16(kv_k)) ||
+      (kv_vt && !aligned16(kv_vt)))
+    return fail(HDF_E_INVALID, "draft_block: tensors must be 16-byte aligned");
+  const DraftPlan P = plan_workspace(*w, n_seq, B, n_new, max_ctx);
+  if (ws == nullptr || ws_bytes < P.total)
+    return fail(HDF_E_WORKSPACE, "draft_block: workspace of %zu bytes needed, %zu given", P.total,
+                ws_bytes);
+  if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0)
+    return fail(HDF_E_INVALID, "draft_block: workspace must be 256-byte aligned");
+
+  const hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const bool bf = w->dtype == HDF_BF16;
+  const int d = w->d, nh = w->n_heads, hd = w->head_dim, F = w->d_ff, L = w->n_layers;
+  const int M = n_seq * B;
+  const size_t el = bf ? 2 : 4;
+  char* base = static_cast<char*>(ws);
+  int32_t* plan_pos = reinterpret_cast<int32_t*>(base + P.plan_pos);
+  int32_t* plan_row = reinterpret_cast<int32_t*>(base + P.plan_row);
+  void* cbuf = base + P.c;
+  float* h = reinterpret_cast<float*>(base + P.h);
+  void* u = base + P.u;
+  void* q = base + P.q;
+  void* kb = base + P.kb;
+  void* vtb = base + P.vtb;
+  float* parts = reinterpret_cast<float*>(base + P.parts);
+  float* part_o = reinterpret_cast<float*>(base + P.part_o);
+  float* part_ml = reinterpret_cast<float*>(base + P.part_ml);
+  void* attn = base + P.attn;
+  void* act = base + P.act;
+  const int64_t capb = int64_t(n_seq) * 64;
+  const size_t layer_kv = size_t(nh) * size_t(kv_cap) * hd * el;  // bytes of one layer's k
+  hipError_t e;
+#define HDF_TRY(x)                                  \
+  do {                                              \
+    e = (x);                                        \
+    if (e != hipSuccess) return hip_fail(e, #x);    \
+  } while (0)
+
+  // Context rows projected in this call: (position, cache row) per row, then in
+  // chunks: c = RMSNorm(y) * ctx_norm and, per layer, K/V into the cache.
+  if (n_new > 0) {
+    HDF_TRY(hdf::launch_plan_rows(ctx_len, new_offsets, kv_offsets, n_seq, n_new, plan_pos,
+                                  plan_row, s));
+    for (int64_t r0 = 0; r0 < n_new; r0 += kCtxChunk) {
+      const int rows = int(n_new - r0 < kCtxChunk ? n_new - r0 : kCtxChunk);
+      HDF_TRY(hdf::launch_row_norm(bf, static_cast<const char*>(y_new) + r0 * d * el, w->ctx_norm,
+                                   w->eps, rows, d, cbuf, s));
+      for (int l = 0; l < L; ++l) {
+        const char* wkv = static_cast<const char*>(w->w_qkv[l]) + size_t(d) * d * el;
+        const int S = hdf::gemm_pick_splits(bf, rows, 2 * d, d);
+        HDF_TRY(hdf::launch_gemm_partial(bf, cbuf, d, wkv, d, rows, 2 * d, d, S, parts, s));
+        hdf::QkvEpiArgs ea{};
+        ea.parts = parts; ea.S = S; ea.M = rows; ea.first_part = 1;
+        ea.d = d; ea.nh = nh; ea.hd = hd; ea.B = B;
+        ea.ctx_len = ctx_len; ea.plan_pos = plan_pos + r0; ea.plan_row = plan_row + r0;
+        ea.rope_cs = w->rope_cs;
+        ea.q = nullptr;
+        ea.k = static_cast<char*>(kv_k) + l * layer_kv;
+        ea.vt = static_cast<char*>(kv_vt) + l * layer_kv;
+        ea.cap = kv_cap;
+        HDF_TRY(hdf::launch_qkv_epilogue(bf, ea, s));
+      }
+    }
+  }
+
+  // Block: h = emb[tokens]; u = RMSNorm(h) * attn_norm[0].
+  HDF_TRY(hdf::launch_embed_norm(bf, tokens, w->tok_emb, w->attn_norm[0], w->eps, M, d, h, u, s));
+  const int n_chunks = (max_ctx + P.chunk_len - 1) / P.chunk_len;
+  for (int l = 0; l < L; ++l) {
+    // Q, K_b, V_b with RoPE at T_s + k.
+    const int Sq = hdf::gemm_pick_splits(bf, M, 3 * d, d);
+    HDF_TRY(hdf::launch_gemm_partial(bf, u, d, w->w_qkv[l], d, M, 3 * d, d, Sq, parts, s));
+    hdf::QkvEpiArgs ea{};
+    ea.parts = parts; ea.S = Sq; ea.M = M; ea.first_part = 0;
+    ea.d = d; ea.nh = nh; ea.hd = hd; ea.B = B;
+    ea.ctx_len = ctx_len; ea.rope_cs = w->rope_cs;
+    ea.q = q; ea.k = kb; ea.vt = vtb; ea.cap = capb;
+    HDF_TRY(hdf::launch_qkv_epilogue(bf, ea, s));
+
+    hdf::AttnArgs aa{};
+    aa.q = q;
+    aa.kc = static_cast<char*>(kv_k) + l * layer_kv;
+    aa.vtc = static_cast<char*>(kv_vt) + l * layer_kv;
+    aa.cap = kv_cap; aa.kv_offsets = kv_offsets; aa.ctx_len = ctx_len;
+    aa.kb = kb; aa.vtb = vtb; aa.capb = capb;
+    aa.n_seq = n_seq; aa.nh = nh; aa.hd = hd; aa.B = B; aa.QB = ((B + 15) / 16) * 16;
+    aa.n_chunks = n_chunks; aa.chunk_len = P.chunk_len;
+    aa.scale_log2 = float(1.4426950408889634 / sqrt(double(hd)));
+    aa.part_o = part_o; aa.part_ml = part_ml;
+    HDF_TRY(hdf::launch_attention(bf, aa, attn, s));
+
+    // h += O Wo^T; u = RMSNorm(h) * mlp_norm.
+    const int So = hdf::gemm_pick_splits(bf, M, d, d);
+    HDF_TRY(hdf::launch_gemm_partial(bf, attn, d, w->w_o[l], d, M, d, d, So, parts, s));
+    HDF_TRY(hdf::launch_residual_norm(bf, parts, So, w->mlp_norm[l], w->eps, M, d, h, u, s));
+
+    // act = SiLU(u Wg^T) * (u Wu^T); h += act Wd^T; next norm.
+    const int Sg = hdf::gemm_pick_splits(bf, M, 2 * F, d);
+    HDF_TRY(hdf::launch_gemm_partial(bf, u, d, w->w_gate_up[l], d, M, 2 * F, d, Sg, parts, s));
+    HDF_TRY(hdf::launch_silu_epilogue(bf, parts, Sg, M, F, act, s));
+    const int Sd = hdf::gemm_pick_splits(bf, M, d, F);
+    HDF_TRY(hdf::launch_gemm_partial(bf, act, F, w->w_down[l], F, M, d, F, Sd, parts, s));
+    const bool last = (l + 1 == L);
+    HDF_TRY(hdf::launch_residual_norm(bf, parts, Sd, last ? w->final_norm : w->attn_norm[l + 1],
+                                      w->eps, M, d, h, last ? hidden : u, s));
+  }
+#undef HDF_TRY
+  return ok();
 }
 
-size_t hdf_lm_head_workspace(int64_t M, int vocab) { return 0; }
+size_t hdf_lm_head_workspace(int64_t M, int vocab) {
+  if (M < 0 || vocab < 1) return 0;
+  return size_t((M * 8 + 255) / 256 * 256);
+}
 
 hdf_status hdf_lm_head_argmax(const void* hidden, const void* W_lm, int64_t M, int d, int vocab,
                               hdf_dtype dtype, int32_t* argmax, float* max_logit, float* logits,
                               void* ws, size_t ws_bytes, hdf_stream_t stream) {
-  return fail(HDF_E_UNSUPPORTED, "lm_head_argmax: not built yet");
+  if (dtype != HDF_F32 && dtype != HDF_BF16) return fail(HDF_E_INVALID, "lm_head: bad dtype");
+  if (M < 0) return fail(HDF_E_INVALID, "lm_head: M < 0");
+  if (d <= 0 || d % 64 != 0) return fail(HDF_E_INVALID, "lm_head: d=%d not a positive multiple of 64", d);
+  if (vocab < 1) return fail(HDF_E_INVALID, "lm_head: vocab < 1");
+  if (M == 0) return ok();
+  if (hidden == nullptr || W_lm == nullptr || argmax == nullptr)
+    return fail(HDF_E_INVALID, "lm_head: null pointer");
+  if (!aligned16(hidden) || !aligned16(W_lm))
+    return fail(HDF_E_INVALID, "lm_head: hidden and W_lm must be 16-byte aligned");
+  const size_t need = hdf_lm_head_workspace(M, vocab);
+  if (ws == nullptr || ws_bytes < need)
+    return fail(HDF_E_WORKSPACE, "lm_head: workspace of %zu bytes needed, %zu given", need, ws_bytes);
+  if ((reinterpret_cast<uintptr_t>(ws) & 7u) != 0)
+    return fail(HDF_E_INVALID, "lm_head: workspace must be 8-byte aligned");
+  hipError_t e = hdf::launch_lm_head(dtype == HDF_BF16, hidden, W_lm, M, d, vocab,
+                                     static_cast<unsigned long long*>(ws), argmax, max_logit,
+                                     logits, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "lm_head launch");
+  return ok();
 }
 
 }  // extern "C"

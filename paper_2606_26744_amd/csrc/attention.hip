@@ -1,0 +1,341 @@
+// Block attention of the one-pass drafter: every block query of a sequence attends
+// to all of that sequence's cached context keys and to all B block keys, with no
+// mask (bidirectional within the block; block slots are predicted jointly from
+// the anchor and the context, Sec. 1 and Sec. 2.1).  Softmax scale 1/sqrt(hd),
+// fp32 softmax with online rescaling.
+//
+// Layouts (one layer): keys K[head][row][hd] (rows of a sequence contiguous),
+// values transposed Vt[head][hd][row] (rows fastest).  The context of sequence s
+// starts at cache row kv_offsets[s]; its block keys sit in a 64-row slot s of
+// separate block buffers of the same layout.
+//
+// bf16 kernel: grid (context chunk + 1 block chunk, head, sequence x 16-query
+// group), 4 waves.  A wave streams 64-key tiles and keeps its 16 queries' state
+// in registers:
+//   S^T (keys x queries) = K . Q^T     v_mfma_f32_16x16x32_bf16, Q as the B operand
+//   O^T (hd x queries)  += V^T . P^T   same instruction, V^T as the A operand, P^T
+//                                      as a bf16 hi + lo pair
+// Keys inside each 32-key step are ordered so that the S^T accumulator a lane
+// holds (4 keys of one query per 16-key sub-tile) is exactly the 8 keys of one
+// query the P^T operand needs, so P never leaves registers; V^T operands are one
+// 16-byte load each from the transposed cache.  No LDS in the key loop.  The four
+// waves of a workgroup merge through LDS at the end; chunks merge in a combine
+// kernel (log-sum-exp rescaling).
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace hdf {
+
+constexpr int kAttnThreads = 256;
+constexpr int kAttnWaves = 4;
+constexpr int kKeyTile = 64;
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+template <int HD>
+__global__ void __launch_bounds__(kAttnThreads)
+attn_bf16_kernel(AttnArgs a) {
+  constexpr int NJ = HD / 32;   // MFMA steps over the head dimension for S
+  constexpr int NDT = HD / 16;  // 16-row tiles of O^T
+  __shared__ float red_o[kAttnWaves][16][HD + 1];
+  __shared__ float red_m[kAttnWaves][16];
+  __shared__ float red_l[kAttnWaves][16];
+
+  const int chunk = blockIdx.x;
+  const int h = blockIdx.y;
+  const int nqg = (a.B + 15) / 16;
+  const int s = blockIdx.z / nqg;
+  const int qg = blockIdx.z - s * nqg;
+  const int lane = threadIdx.x & 63;
+  const int wid = threadIdx.x >> 6;
+  const int g = lane >> 4;       // lane group 0..3
+  const int ql = lane & 15;      // query within the group / row within a sub-tile
+  const int T = a.ctx_len[s];
+
+  const bf16_t* kbase;
+  const bf16_t* vbase;
+  int64_t vstride;
+  int k_lo, k_hi;
+  if (chunk < a.n_chunks) {
+    k_lo = chunk * a.chunk_len;
+    if (k_lo >= T) return;  // nothing of this sequence in this chunk
+    k_hi = min(T, k_lo + a.chunk_len);
+    const int64_t row0 = a.kv_offsets[s];
+    kbase = static_cast<const bf16_t*>(a.kc) + (int64_t(h) * a.cap + row0) * HD;
+    vbase = static_cast<const bf16_t*>(a.vtc) + int64_t(h) * HD * a.cap + row0;
+    vstride = a.cap;
+  } else {
+    k_lo = 0;
+    k_hi = a.B;
+    const int64_t row0 = int64_t(s) * 64;
+    kbase = static_cast<const bf16_t*>(a.kb) + (int64_t(h) * a.capb + row0) * HD;
+    vbase = static_cast<const bf16_t*>(a.vtb) + int64_t(h) * HD * a.capb + row0;
+    vstride = a.capb;
+  }
+
+  // Q^T operand: lane holds Q[query ql][32j + 8g .. +7].
+  const int q = qg * 16 + ql;
+  bf16x8_t qf[NJ];
+  {
+    const bf16_t* qrow = static_cast<const bf16_t*>(a.q) + ((int64_t(s) * a.nh + h) * a.B + q) * HD;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      u32x4 v = (q < a.B) ? ld16(qrow + 32 * j + 8 * g) : u32x4{0, 0, 0, 0};
+      qf[j] = __builtin_bit_cast(bf16x8_t, v);
+    }
+  }
+
+  f32x4_t oacc[NDT];
+#pragma unroll
+  for (int i = 0; i < NDT; ++i) oacc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY;
+  float l_run = 0.f;
+
+  for (int t0 = k_lo + wid * kKeyTile; t0 < k_hi; t0 += kAttnWaves * kKeyTile) {
+    // K operands of the four 16-key sub-tiles: sub-tile st = 2*ks + p, row r -> key
+    // t0 + 32ks + 8(r/4) + 4p + r%4.
+    bf16x8_t kf[4][NJ];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      const int key = t0 + 32 * (st >> 1) + 8 * (ql >> 2) + 4 * (st & 1) + (ql & 3);
+      const bf16_t* krow = kbase + int64_t(key) * HD + 8 * g;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) kf[st][j] = __builtin_bit_cast(bf16x8_t, ld16(krow + 32 * j));
+    }
+    // V^T operands: lane holds V^T[16dt + ql][t0 + 32ks + 8g .. +7].
+    u32x4 vf[2][NDT];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+        vf[ks][dt] = ld16(vbase + int64_t(16 * dt + ql) * vstride + t0 + 32 * ks + 8 * g);
+
+    float sv[4][4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[st][j], qf[j], acc, 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = t0 + 32 * (st >> 1) + 8 * g + 4 * (st & 1) + i;
+        sv[st][i] = (key < k_hi) ? acc[i] * a.scale_log2 : -INFINITY;
+      }
+    }
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) tmax = fmaxf(tmax, sv[st][i]);
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
+    const float m_new = fmaxf(m_run, tmax);   // finite: every tile has a valid key
+    const float alpha = fast_exp2(m_run - m_new);
+    m_run = m_new;
+    float psum = 0.f;
+    float pv[4][4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        pv[st][i] = fast_exp2(sv[st][i] - m_new);
+        psum += pv[st][i];
+      }
+    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) oacc[dt][i] *= alpha;
+
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      // P^T operand: keys 32ks + 8g + 0..7 of query ql, as a bf16 pair hi + lo
+      // (P carries ~16 significant bits into the fp32 accumulation; the key loop is
+      // HBM-bound, so the second MFMA is free).
+      float pk[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        pk[i] = pv[2 * ks][i];
+        pk[4 + i] = pv[2 * ks + 1][i];
+      }
+      uint32_t hw[4], lw[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bf16_t h0 = f2bf(pk[2 * e]), h1 = f2bf(pk[2 * e + 1]);
+        hw[e] = uint32_t(h0) | (uint32_t(h1) << 16);
+        lw[e] = pack_bf2(pk[2 * e] - bf2f(h0), pk[2 * e + 1] - bf2f(h1));
+      }
+      const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, u32x4{hw[0], hw[1], hw[2], hw[3]});
+      const bf16x8_t pf_lo = __builtin_bit_cast(bf16x8_t, u32x4{lw[0], lw[1], lw[2], lw[3]});
+      // Keys past the segment end carry P = 0; zero their V too (the slot padding
+      // is never written and may hold anything).
+      const int kfirst = t0 + 32 * ks + 8 * g;
+      const int nvalid = k_hi - kfirst;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        u32x4 v = vf[ks][dt];
+        if (nvalid < 8) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t keep_lo = (2 * e < nvalid) ? 0x0000FFFFu : 0u;
+            const uint32_t keep_hi = (2 * e + 1 < nvalid) ? 0xFFFF0000u : 0u;
+            v[e] &= (keep_lo | keep_hi);
+          }
+        }
+        const bf16x8_t vop = __builtin_bit_cast(bf16x8_t, v);
+        oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pf, oacc[dt], 0, 0, 0);
+        oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pf_lo, oacc[dt], 0, 0, 0);
+      }
+    }
+  }
+
+  // Wave -> LDS: lane (g, ql) holds O^T[16dt + 4g + i][ql].
+  l_run += __shfl_xor(l_run, 16, kWave);
+  l_run += __shfl_xor(l_run, 32, kWave);
+  if (g == 0) {
+    red_m[wid][ql] = m_run;
+    red_l[wid][ql] = l_run;
+  }
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red_o[wid][ql][16 * dt + 4 * g + i] = oacc[dt][i];
+  __syncthreads();
+
+  const int64_t pidx = ((int64_t(s) * a.nh + h) * (a.n_chunks + 1) + chunk) * a.QB + qg * 16;
+  for (int e = threadIdx.x; e < 16 * HD; e += kAttnThreads) {
+    const int qq = e / HD, dim = e - qq * HD;
+    float mm = red_m[0][qq];
+#pragma unroll
+    for (int w = 1; w < kAttnWaves; ++w) mm = fmaxf(mm, red_m[w][qq]);
+    float o = 0.f, l = 0.f;
+#pragma unroll
+    for (int w = 0; w < kAttnWaves; ++w) {
+      const float f = (red_m[w][qq] == -INFINITY) ? 0.f : fast_exp2(red_m[w][qq] - mm);
+      o += f * red_o[w][qq][dim];
+      l += f * red_l[w][qq];
+    }
+    a.part_o[(pidx + qq) * HD + dim] = o;
+    if (dim == 0) {
+      a.part_ml[(pidx + qq) * 2 + 0] = mm;
+      a.part_ml[(pidx + qq) * 2 + 1] = l;
+    }
+  }
+}
+
+// Merge the chunk partials of one (sequence, head, 16-query group) -> O rows.
+template <typename T>
+__global__ void __launch_bounds__(kAttnThreads)
+attn_combine_kernel(AttnArgs a, T* __restrict__ out) {
+  const int h = blockIdx.y;
+  const int nqg = (a.B + 15) / 16;
+  const int s = blockIdx.x / nqg;
+  const int qg = blockIdx.x - s * nqg;
+  const int T_s = a.ctx_len[s];
+  const int nc = min(a.n_chunks, (T_s + a.chunk_len - 1) / a.chunk_len);
+  const int d = a.nh * a.hd;
+  for (int e = threadIdx.x; e < 16 * a.hd; e += kAttnThreads) {
+    const int qq = e / a.hd, dim = e - qq * a.hd;
+    const int q = qg * 16 + qq;
+    if (q >= a.B) continue;
+    const int64_t base = (int64_t(s) * a.nh + h) * (a.n_chunks + 1);
+    float mm = -INFINITY;
+    for (int c = 0; c <= nc; ++c) {
+      const int cc = (c == nc) ? a.n_chunks : c;
+      mm = fmaxf(mm, a.part_ml[((base + cc) * a.QB + q) * 2]);
+    }
+    float o = 0.f, l = 0.f;
+    for (int c = 0; c <= nc; ++c) {
+      const int cc = (c == nc) ? a.n_chunks : c;
+      const int64_t pi = (base + cc) * a.QB + q;
+      const float mc = a.part_ml[pi * 2];
+      const float f = (mc == -INFINITY) ? 0.f : fast_exp2(mc - mm);
+      o += f * a.part_o[pi * a.hd + dim];
+      l += f * a.part_ml[pi * 2 + 1];
+    }
+    const float v = o / l;
+    T* dst = out + (int64_t(s) * a.B + q) * d + int64_t(h) * a.hd + dim;
+    if constexpr (sizeof(T) == 2)
+      *dst = f2bf(v);
+    else
+      *dst = v;
+  }
+}
+
+// fp32 path (small correctness-size workloads): one thread per query, keys streamed
+// from the same layouts, exact expf softmax with online rescaling.
+template <int HD>
+__global__ void attn_f32_kernel(AttnArgs a, float* __restrict__ out) {
+  const int s = blockIdx.x, h = blockIdx.y;
+  const int q = threadIdx.x;
+  if (q >= a.B) return;
+  constexpr int hd = HD;
+  const int d = a.nh * hd;
+  const float* Q = static_cast<const float*>(a.q) + ((int64_t(s) * a.nh + h) * a.B + q) * hd;
+  const float scale = rsqrtf(float(hd));
+  float o[HD];
+#pragma unroll
+  for (int i = 0; i < hd; ++i) o[i] = 0.f;
+  float m = -INFINITY, l = 0.f;
+  for (int seg = 0; seg < 2; ++seg) {
+    const float* K;
+    const float* Vt;
+    int64_t vs;
+    int n;
+    if (seg == 0) {
+      const int64_t row0 = a.kv_offsets[s];
+      K = static_cast<const float*>(a.kc) + (int64_t(h) * a.cap + row0) * hd;
+      Vt = static_cast<const float*>(a.vtc) + int64_t(h) * hd * a.cap + row0;
+      vs = a.cap;
+      n = a.ctx_len[s];
+    } else {
+      const int64_t row0 = int64_t(s) * 64;
+      K = static_cast<const float*>(a.kb) + (int64_t(h) * a.capb + row0) * hd;
+      Vt = static_cast<const float*>(a.vtb) + int64_t(h) * hd * a.capb + row0;
+      vs = a.capb;
+      n = a.B;
+    }
+    for (int j = 0; j < n; ++j) {
+      float sc = 0.f;
+      for (int i = 0; i < hd; ++i) sc = fmaf(Q[i], K[int64_t(j) * hd + i], sc);
+      sc *= scale;
+      const float mn = fmaxf(m, sc);
+      const float al = expf(m - mn);
+      const float p = expf(sc - mn);
+      l = l * al + p;
+#pragma unroll
+      for (int i = 0; i < hd; ++i) o[i] = o[i] * al + p * Vt[int64_t(i) * vs + j];
+      m = mn;
+    }
+  }
+  float* dst = out + (int64_t(s) * a.B + q) * d + int64_t(h) * hd;
+#pragma unroll
+  for (int i = 0; i < hd; ++i) dst[i] = o[i] / l;
+}
+
+hipError_t launch_attention(bool bf16, const AttnArgs& a, void* out, hipStream_t s) {
+  if (a.n_seq <= 0) return hipSuccess;
+  if (!bf16) {
+    if (a.hd == 128)
+      hipLaunchKernelGGL(attn_f32_kernel<128>, dim3(a.n_seq, a.nh), dim3(64), 0, s, a,
+                         static_cast<float*>(out));
+    else
+      hipLaunchKernelGGL(attn_f32_kernel<64>, dim3(a.n_seq, a.nh), dim3(64), 0, s, a,
+                         static_cast<float*>(out));
+    return hipGetLastError();
+  }
+  const int nqg = (a.B + 15) / 16;
+  const dim3 grid(a.n_chunks + 1, a.nh, a.n_seq * nqg);
+  if (a.hd == 128)
+    hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(kAttnThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(kAttnThreads), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(attn_combine_kernel<bf16_t>, dim3(a.n_seq * nqg, a.nh), dim3(kAttnThreads), 0,
+                     s, a, static_cast<bf16_t*>(out));
+  return hipGetLastError();
+}
+
+}  // namespace hdf

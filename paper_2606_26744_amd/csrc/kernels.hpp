@@ -24,4 +24,82 @@ hipError_t launch_accept(const int32_t* draft, int stride, const int32_t* target
                          int K, int32_t* acc, int32_t* anchor, int32_t* offs, int32_t* toks,
                          hipStream_t s);
 
+// ---------------------------------------------------------------- GEMM (gemm.hip)
+constexpr int kEpiPartial = 0;  // fp32 C / split-K partials
+constexpr int kEpiArgmax = 1;   // LM head: fused row argmax (+ optional fp32 logits in C)
+
+struct GemmArgs {
+  const void* A;
+  int64_t lda;
+  const void* B;
+  int64_t ldb;
+  int M, N, K;
+  float* C;
+  unsigned long long* keys;
+};
+
+int gemm_k_align(bool bf16);                       // K must be a multiple of this
+int gemm_pick_splits(bool bf16, int M, int N, int K);
+// C[z][M][N] (fp32) = A[M][K] . B[N][K]^T over the z-th of `splits` K ranges.
+hipError_t launch_gemm_partial(bool bf16, const void* A, int64_t lda, const void* B, int64_t ldb,
+                               int M, int N, int K, int splits, float* C, hipStream_t s);
+// keys: M 64-bit scratch words.  logits may be NULL.
+hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t M, int d, int V,
+                          unsigned long long* keys, int32_t* argmax, float* max_logit,
+                          float* logits, hipStream_t s);
+
+// ---------------------------------------------------------------- row-wise (rowwise.hip)
+struct QkvEpiArgs {
+  const float* parts;    // [S][M][n_parts*d]
+  int S, M;
+  int first_part;        // 0: parts are Q,K,V (block rows); 1: parts are K,V (context rows)
+  int d, nh, hd, B;
+  const int32_t* ctx_len;   // block rows: position = ctx_len[s] + k
+  const int32_t* plan_pos;  // context rows: position and cache row per row
+  const int32_t* plan_row;
+  const float* rope_cs;     // [pos][hd/2][2] or NULL
+  void* q;                  // block rows: [n_seq][nh][B][hd]
+  void* k;                  // [nh][cap][hd]
+  void* vt;                 // [nh][hd][cap]
+  int64_t cap;
+};
+
+hipError_t launch_plan_rows(const int32_t* ctx_len, const int32_t* new_offsets,
+                            const int32_t* kv_offsets, int n_seq, int64_t n_new, int32_t* plan_pos,
+                            int32_t* plan_row, hipStream_t s);
+// out = RMSNorm(in) * gamma, row-wise, in/out in the working dtype.
+hipError_t launch_row_norm(bool bf16, const void* in, const float* gamma, float eps, int64_t rows,
+                           int d, void* out, hipStream_t s);
+// h = float(emb[tokens]); u = RMSNorm(h) * gamma
+hipError_t launch_embed_norm(bool bf16, const int32_t* tokens, const void* emb, const float* gamma,
+                             float eps, int64_t rows, int d, float* h, void* u, hipStream_t s);
+// h += sum_z parts[z]; u = RMSNorm(h) * gamma
+hipError_t launch_residual_norm(bool bf16, const float* parts, int S, const float* gamma, float eps,
+                                int64_t rows, int d, float* h, void* u, hipStream_t s);
+hipError_t launch_qkv_epilogue(bool bf16, const QkvEpiArgs& a, hipStream_t s);
+// act = SiLU(gate) * up from parts [S][M][2F] (gate columns first)
+hipError_t launch_silu_epilogue(bool bf16, const float* parts, int S, int64_t M, int F, void* act,
+                                hipStream_t s);
+
+// ---------------------------------------------------------------- attention (attention.hip)
+struct AttnArgs {
+  const void* q;             // [n_seq][nh][B][hd]
+  const void* kc;            // layer's context keys   [nh][cap][hd]
+  const void* vtc;           // layer's context values [nh][hd][cap]
+  int64_t cap;
+  const int32_t* kv_offsets; // [n_seq+1] cache slot of each sequence
+  const int32_t* ctx_len;    // [n_seq]
+  const void* kb;            // block keys   [nh][capb][hd], slot s at row 64*s
+  const void* vtb;           // block values [nh][hd][capb]
+  int64_t capb;
+  int n_seq, nh, hd, B, QB;  // QB = B rounded up to 16
+  int n_chunks, chunk_len;   // context chunks of the grid (chunk_len % 64 == 0)
+  float scale_log2;          // log2(e) / sqrt(hd)
+  float* part_o;             // [n_seq][nh][n_chunks+1][QB][hd]
+  float* part_ml;            // [n_seq][nh][n_chunks+1][QB][2]
+};
+
+// out: [n_seq*B][nh*hd] attention output rows in the working dtype.
+hipError_t launch_attention(bool bf16, const AttnArgs& a, void* out, hipStream_t s);
+
 }  // namespace hdf

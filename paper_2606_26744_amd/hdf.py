@@ -233,6 +233,7 @@ class DrafterHandle:
             rope_max_pos if self.rope is not None else 0)
         self._keep = keep
         self.d, self.nh, self.hd, self.F, self.V = d, n_heads, head_dim, d_ff, vocab
+        self.eps = eps
 
     def kv_cache_bytes(self, kv_cap: int) -> int:
         return int(lib().hdf_kv_cache_bytes(ctypes.byref(self.s), kv_cap))

@@ -246,6 +246,12 @@ def kv_prefix(wl: Workload, n_rows: int, layer: int, *, device="cpu", sub: int =
     return k, v
 
 
+def reduced_states(wl: Workload, n_rows: int, *, device="cpu", sub: int = 0) -> torch.Tensor:
+    """Stand-in reduced context states [n_rows, d] for drafter-only tests: N(0, 1), the
+    scale of a gated sum of unit-variance paths with gates near 1/2."""
+    return normal([n_rows, wl.d], 1.0, wl.seed, _TID["H_ctx"], sub, dtype=wl.dtype, device=device)
+
+
 def make_targets(drafts: np.ndarray, match_p: Sequence[float], vocab: int, seed: int,
                  sub: int = 0) -> np.ndarray:
     """Synthetic target-model tokens for greedy verification.

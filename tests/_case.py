@@ -1,0 +1,86 @@
+"""Builds drafter test cases on the GPU and the matching oracle inputs (host copies of
+the very same bits)."""
+import dataclasses
+
+import numpy as np
+import torch
+
+import synth
+from oracle.drafter import Weights
+from paper_2606_26744_amd import hdf
+
+
+def bits(t):
+    return synth.to_numpy_bits(t)
+
+
+class DraftCase:
+    """ctx[s] context length of sequence s; new[s] rows of it projected by this call (the
+    last ones); the rows before come from a synthetic already-filled cache."""
+
+    def __init__(self, wl, ctx, new, *, B=None, random_norms=True, rope=True, sub=0,
+                 max_ctx=None, y_from=None):
+        self.wl = wl = dataclasses.replace(wl, n_seq=len(ctx), ctx_lens=list(ctx),
+                                           block=B or wl.block)
+        dr = wl.drafter
+        self.B = wl.block
+        self.ctx = list(ctx)
+        self.new = list(new)
+        self.max_ctx = max_ctx if max_ctx is not None else max(self.ctx)
+        dev = "cuda"
+        self.w = synth.drafter_weights(wl, device=dev, random_norms=random_norms)
+        theta = dr.rope_theta if rope else 0.0
+        self.h = hdf.DrafterHandle(self.w, n_layers=dr.n_layers, d=dr.d, n_heads=dr.n_heads,
+                                   head_dim=dr.head_dim, d_ff=dr.d_ff, vocab=dr.vocab, eps=dr.eps,
+                                   rope_theta=theta, rope_max_pos=self.max_ctx + self.B)
+        self.theta = theta
+        offs = hdf.kv_slot_offsets(self.ctx)
+        self.kv_offsets = torch.tensor(offs, dtype=torch.int32, device=dev)
+        self.cap = offs[-1]
+        self.kv_k, self.kv_vt = self.h.alloc_kv(max(self.cap, 64))
+        self.ctx_len = torch.tensor(self.ctx, dtype=torch.int32, device=dev)
+        nh, hd, L = dr.n_heads, dr.head_dim, dr.n_layers
+        self.prefix = []
+        for s, (T, n) in enumerate(zip(self.ctx, self.new)):
+            t0 = T - n
+            per_layer = []
+            for l in range(L):
+                if t0 > 0:
+                    k, v = synth.kv_prefix(wl, t0, l, device=dev, sub=sub * 1000 + s)
+                    o = offs[s]
+                    self.kv_k[l, :, o:o + t0, :] = k.view(t0, nh, hd).permute(1, 0, 2)
+                    self.kv_vt[l, :, :, o:o + t0] = v.view(t0, nh, hd).permute(1, 2, 0)
+                    per_layer.append((bits(k), bits(v)))
+                else:
+                    per_layer.append((np.zeros((0, dr.d)), np.zeros((0, dr.d))))
+            self.prefix.append(per_layer)
+        no = [0]
+        for n in self.new:
+            no.append(no[-1] + n)
+        self.new_offsets = torch.tensor(no, dtype=torch.int32, device=dev)
+        self.n_new = no[-1]
+        self.y_new = (synth.reduced_states(wl, self.n_new, device=dev, sub=sub) if y_from is None
+                      else y_from)
+        self.tokens = synth.block_tokens(wl, device=dev, sub=sub)
+
+    def run(self, hidden=None, ws=None):
+        return self.h.draft_block(ctx_len=self.ctx_len, max_ctx=self.max_ctx, y_new=self.y_new,
+                                  new_offsets=self.new_offsets, kv_offsets=self.kv_offsets,
+                                  kv_k=self.kv_k, kv_vt=self.kv_vt, tokens=self.tokens,
+                                  hidden=hidden, ws=ws)
+
+    def oracle_weights(self):
+        dr = self.wl.drafter
+        wb = {k: ([bits(x) for x in v] if isinstance(v, list) else bits(v))
+              for k, v in self.w.items()}
+        return Weights(wb, d=dr.d, n_layers=dr.n_layers, n_heads=dr.n_heads, head_dim=dr.head_dim,
+                       d_ff=dr.d_ff, vocab=dr.vocab, eps=dr.eps, rope_theta=self.theta,
+                       dtype=self.wl.dtype)
+
+    def y_rows(self, s):
+        no = self.new_offsets.tolist()
+        return bits(self.y_new[no[s]:no[s + 1]])
+
+    def oracle_inputs(self):
+        ys = [self.y_rows(s) for s in range(len(self.ctx))]
+        return ys, bits(self.tokens)

@@ -1,0 +1,115 @@
+"""GPU parity of hdf_draft_block (the one-pass block drafter) against the CPU oracle:
+final-normed block states and the KV-cache rows it writes."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle.drafter import context_kv, draft_block as ref_draft
+from oracle.numerics import as_f64
+from tests._case import DraftCase, bits
+from tests._tol import assert_bf16_state_close, assert_f32_rows_close
+
+pytestmark = pytest.mark.gpu
+
+
+def _compare(case, seqs=None, check_cache=True):
+    print(f"[draft_block] {case.wl.name} dtype={case.wl.dtype} ctx={case.ctx[:6]} "
+          f"new={case.new[:6]} B={case.B} seqs={seqs}", flush=True)
+    hidden = case.run()
+    torch.cuda.synchronize()
+    W = case.oracle_weights()
+    ys, toks = case.oracle_inputs()
+    seqs = list(range(len(case.ctx))) if seqs is None else list(seqs)
+    ref = ref_draft(W, ys, toks, kv_prefix=case.prefix, seqs=seqs)
+    B = case.B
+    got = np.concatenate([bits(hidden[s * B:(s + 1) * B]) for s in seqs])
+    if case.wl.dtype == "bf16":
+        flips, worst = assert_bf16_state_close(as_f64(got), ref, "hidden")
+        print(f"  hidden: {flips} of {ref.size} elements differ; worst row RMS rel {worst:.2e}",
+              flush=True)
+    else:
+        assert_f32_rows_close(got, ref, "hidden")
+    if check_cache:
+        offs = case.kv_offsets.tolist()
+        dr = case.wl.drafter
+        for s in seqs[:3]:
+            T, n = case.ctx[s], case.new[s]
+            if n == 0:
+                continue
+            kv = context_kv(W, as_f64(case.y_rows(s)), np.arange(T - n, T))
+            for l in range(dr.n_layers):
+                k = case.kv_k[l, :, offs[s] + T - n:offs[s] + T, :].permute(1, 0, 2).reshape(n, -1)
+                v = case.kv_vt[l, :, :, offs[s] + T - n:offs[s] + T].permute(2, 0, 1).reshape(n, -1)
+                if case.wl.dtype == "bf16":
+                    assert_bf16_state_close(as_f64(bits(k.contiguous())), kv[l][0], "cache K")
+                    assert_bf16_state_close(as_f64(bits(v.contiguous())), kv[l][1], "cache V")
+                else:
+                    assert_f32_rows_close(k.cpu().numpy(), kv[l][0], "cache K")
+                    assert_f32_rows_close(v.cpu().numpy(), kv[l][1], "cache V")
+    return hidden
+
+
+def test_tiny_fp32_cold():
+    wl = synth.tiny_fp32()
+    _compare(DraftCase(wl, [64], [64]))
+
+
+def test_small_bf16_cold_and_warm():
+    wl = synth.small_bf16()
+    _compare(DraftCase(wl, [512] * 4, [512] * 4))
+    _compare(DraftCase(wl, [512] * 4, [16] * 4, sub=1))
+
+
+def test_ragged_lengths_and_two_query_groups():
+    wl = synth.small_bf16()
+    ctx = [1, 63, 64, 65, 200, 513, 1030]
+    new = [1, 5, 64, 16, 0, 513, 7]
+    _compare(DraftCase(wl, ctx, new, B=20, sub=2))
+
+
+def test_block_of_one():
+    wl = synth.small_bf16()
+    _compare(DraftCase(wl, [100, 7], [100, 7], B=1, sub=3))
+
+
+def test_head_dim_128_and_loose_max_ctx():
+    wl = synth.small_bf16()
+    wl.drafter = synth.DrafterShape(d=512, n_layers=1, n_heads=4, head_dim=128, d_ff=1024,
+                                    vocab=1000)
+    wl.d = 512
+    _compare(DraftCase(wl, [300, 1500, 64], [20, 1500, 64], sub=4, max_ctx=3000))
+
+
+def test_no_rope_fp32_multilayer():
+    wl = synth.tiny_fp32()
+    wl.drafter = synth.DrafterShape(d=256, n_layers=3, n_heads=4, head_dim=64, d_ff=512,
+                                    vocab=500)
+    _compare(DraftCase(wl, [40, 9], [10, 9], rope=False, sub=5))
+
+
+def test_full_size_warm_sampled():
+    """Full-size warm step: 8 sequences x 2048 context, 16 new rows each; the oracle
+    evaluates two sequences."""
+    wl = synth.drafter_full()
+    case = DraftCase(wl, [2048] * 8, [16] * 8, random_norms=False)
+    _compare(case, seqs=[0, 5])
+    del case
+    torch.cuda.empty_cache()
+
+
+def test_ragged_long_contexts_sampled():
+    wl = synth.ragged_decode()
+    ctx = [1024, 16384, 5000, 777 + 1024]
+    case = DraftCase(wl, ctx, [16] * 4, random_norms=False, sub=6, max_ctx=16384)
+    _compare(case, seqs=[1, 3])
+    del case
+    torch.cuda.empty_cache()
+
+
+def test_determinism():
+    wl = synth.small_bf16()
+    case = DraftCase(wl, [700, 300], [16, 300], sub=7)
+    h1 = case.run().clone()
+    h2 = case.run().clone()
+    assert torch.equal(h1, h2)

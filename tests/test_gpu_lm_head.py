@@ -1,0 +1,97 @@
+"""GPU parity of hdf_lm_head_argmax (draft logits and greedy tokens, Sec. 2.3) against
+the CPU oracle.  Argmax is bit-exact except on rows whose oracle top-2 margin is
+below 1e-2; logits within 1e-4 relative (fp32) or 2e-2 absolute (bf16)."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle.lm_head import lm_head_argmax as ref_lm
+from paper_2606_26744_amd import hdf
+from tests._tol import assert_abs_close, assert_f32_rows_close
+
+pytestmark = pytest.mark.gpu
+MARGIN = 1e-2
+
+
+def _inputs(M, d, V, dtype, seed):
+    wl = synth.Workload("lm", dtype, seed, m=4, d=d)
+    hid = synth.normal([M, d], 1.0, seed, 50, dtype=dtype, device="cuda")   # unit-RMS states
+    w = synth.normal([V, d], 0.02, seed, 51, dtype=dtype, device="cuda")
+    return hid, w
+
+
+def _check(hid, w, rows=None, want_logits=True, dtype="bf16"):
+    M, V = hid.shape[0], w.shape[0]
+    print(f"[lm_head] M={M} d={hid.shape[1]} V={V} dtype={dtype}", flush=True)
+    am, mx, lg = hdf.lm_head_argmax(hid, w, want_logits=want_logits)
+    torch.cuda.synchronize()
+    sel = np.arange(M) if rows is None else np.asarray(rows)
+    r_am, r_lg, r_margin = ref_lm(synth.to_numpy_bits(hid)[sel], synth.to_numpy_bits(w))
+    g_am = am.cpu().numpy()[sel]
+    ok = r_margin >= MARGIN
+    assert ok.mean() > 0.8
+    assert np.array_equal(g_am[ok], r_am[ok]), np.nonzero(g_am[ok] != r_am[ok])
+    # the GPU's own max logit equals the logit at its argmax, and is the row max
+    g_mx = mx.cpu().numpy()[sel]
+    if want_logits:
+        g_lg = lg.cpu().numpy()[sel]
+        if dtype == "bf16":
+            assert_abs_close(g_lg, r_lg, 2e-2, "logits")
+        else:
+            assert_f32_rows_close(g_lg, r_lg, "logits")
+        assert np.array_equal(g_mx, g_lg.max(axis=1))
+        assert np.array_equal(g_am, np.argmax(g_lg, axis=1))   # fused argmax = argmax of its logits
+    assert_abs_close(g_mx, r_lg.max(axis=1), 2e-2 if dtype == "bf16" else 1e-4, "max logit")
+    return am, mx
+
+
+def test_tiny_fp32():
+    hid, w = _inputs(8, 256, 4096, "f32", 60)
+    _check(hid, w, dtype="f32")
+
+
+@pytest.mark.parametrize("M,d,V", [(64, 1024, 32000), (1, 1024, 1000), (130, 512, 1000),
+                                   (16, 64, 129)])
+def test_bf16_shapes(M, d, V):
+    hid, w = _inputs(M, d, V, "bf16", M + V)
+    _check(hid, w)
+
+
+def test_full_vocab_block_rows():
+    """The full-size step's LM head: 8 sequences x 16 slots, d=4096, V=129280."""
+    hid, w = _inputs(128, 4096, 129280, "bf16", 61)
+    _check(hid, w, rows=list(range(0, 128, 4)) + [127], want_logits=False)
+    torch.cuda.empty_cache()
+
+
+def test_ragged_batch_rows_sampled():
+    """64 sequences x 16 slots (M=1024): 8 M-tiles; sampled rows."""
+    hid, w = _inputs(1024, 4096, 129280, "bf16", 62)
+    _check(hid, w, rows=[0, 1, 127, 128, 500, 1023], want_logits=False)
+    torch.cuda.empty_cache()
+
+
+def test_ties_take_lowest_index():
+    d, V = 128, 3000
+    hid, w = _inputs(4, d, V, "bf16", 63)
+    w[2999] = w[17]
+    w[1200] = w[17]
+    hid[0] = (w[17].float() * 40).to(torch.bfloat16)   # row 0's maximum is the tied row
+    am, _, lg = hdf.lm_head_argmax(hid, w, want_logits=True)
+    assert am[0].item() == 17
+    assert lg[0, 17].item() == lg[0, 1200].item() == lg[0, 2999].item()
+
+
+def test_empty():
+    hid = torch.empty((0, 128), dtype=torch.bfloat16, device="cuda")
+    w = torch.zeros((10, 128), dtype=torch.bfloat16, device="cuda")
+    am, _, _ = hdf.lm_head_argmax(hid, w)
+    assert am.numel() == 0
+
+
+def test_determinism():
+    hid, w = _inputs(128, 1024, 32000, "bf16", 64)
+    a1, m1, l1 = hdf.lm_head_argmax(hid, w, want_logits=True)
+    a2, m2, l2 = hdf.lm_head_argmax(hid, w, want_logits=True)
+    assert torch.equal(a1, a2) and torch.equal(m1, m2) and torch.equal(l1, l2)

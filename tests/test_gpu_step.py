@@ -1,0 +1,129 @@
+"""End-to-end parity of one drafter step (reduce -> draft block -> LM head argmax ->
+accept) on the GPU against the oracle chain on the CPU.
+
+The LM head alone meets 2e-2 on logits and exact argmax outside 1e-2 margins
+(test_gpu_lm_head).  Across a whole step the bf16 storage chain spreads correct results
+further apart (tests/test_bf16_chain_sensitivity.py), so here logits are held to
+E2E_LOGIT_ABS and argmax tokens are compared bit-exactly where the oracle's top-2 margin
+clears E2E_MARGIN; an acceptance length is compared only when every draft position it
+depends on clears that margin.  fp32 workloads keep the 1e-4 relative bounds and 1e-2
+margins."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle.accept import accept as ref_accept
+from oracle.lm_head import lm_head_argmax as ref_lm
+from oracle.drafter import draft_block as ref_draft
+from oracle.reducer import hc_reduce as ref_reduce
+from oracle.numerics import as_f64
+from paper_2606_26744_amd import hdf
+from paper_2606_26744_amd.step import StepBuffers, drafter_step
+from tests._case import DraftCase, bits
+from tests._tol import (E2E_LOGIT_ABS, E2E_MARGIN, assert_abs_close, assert_bf16_close,
+                        assert_bf16_state_close, assert_f32_rows_close)
+
+pytestmark = pytest.mark.gpu
+
+
+def _step_case(wl, ctx, new, *, seqs, sub=0, uniform_targets=False):
+    print(f"[step] {wl.name} ctx={ctx[:6]} new={new[:6]} seqs={seqs}", flush=True)
+    n_new = sum(new)
+    red = synth.reducer_inputs(wl, n_new, device="cuda", sub=sub)
+    case = DraftCase(wl, ctx, new, random_norms=False, sub=sub,
+                     y_from=torch.empty((n_new, wl.d), dtype=red["H"].dtype, device="cuda"))
+    B = case.B
+    n_seq = len(ctx)
+    W = case.oracle_weights()
+    no = case.new_offsets.tolist()
+    Hn = bits(red["H"])
+    Wg, bg = bits(red["W_g"]), bits(red["b_g"])
+    # Oracle chain for the sampled sequences: reduce -> draft block -> LM head.
+    ys = {s: ref_reduce(Hn[no[s]:no[s + 1]], Wg, bg, dtype=wl.dtype)[0] for s in seqs}
+    toks = bits(case.tokens)
+    hid_ref = ref_draft(W, [ys.get(s) for s in range(n_seq)], toks, kv_prefix=case.prefix,
+                        seqs=seqs)
+    am_ref, lg_ref, margin = ref_lm(hid_ref, bits(case.w["w_lm"]))
+    drafts_ref = am_ref.reshape(len(seqs), B)[:, 1:]
+    # Targets: sampled sequences copy the oracle's drafts with the workload's probability;
+    # the others get uniform tokens (they are not checked).
+    V = wl.drafter.vocab
+    rng = np.random.default_rng([wl.seed, 99, sub])
+    targets = rng.integers(0, V, (n_seq, B)).astype(np.int32)
+    if not uniform_targets:
+        p = [(wl.match_p or [0.8] * n_seq)[s] for s in seqs]
+        targets[seqs] = synth.make_targets(drafts_ref, p, V, seed=wl.seed, sub=sub)
+    tg = torch.as_tensor(targets).cuda()
+    bufs = StepBuffers(case.h, n_seq, B, n_new, case.max_ctx, wl.m)
+    out = drafter_step(case.h, bufs, H_new=red["H"], W_g=red["W_g"], b_g=red["b_g"],
+                       new_offsets=case.new_offsets, ctx_len=case.ctx_len, max_ctx=case.max_ctx,
+                       kv_offsets=case.kv_offsets, kv_k=case.kv_k, kv_vt=case.kv_vt,
+                       tokens=case.tokens, targets=tg, logits=True)
+    torch.cuda.synchronize()
+    # Reduced rows
+    for s in seqs:
+        y = bits(out["Y"][no[s]:no[s + 1]])
+        if wl.dtype == "bf16":
+            assert_bf16_close(as_f64(y), ys[s], "Y")
+        else:
+            assert_f32_rows_close(y, ys[s], "Y")
+    rows = np.concatenate([np.arange(s * B, (s + 1) * B) for s in seqs])
+    hid = bits(out["hidden"][torch.as_tensor(rows).cuda()])
+    lg = out["logits"][torch.as_tensor(rows).cuda()].cpu().numpy()
+    if wl.dtype == "bf16":
+        assert_bf16_state_close(as_f64(hid), hid_ref, "hidden")
+        assert_abs_close(lg, lg_ref, E2E_LOGIT_ABS, "logits")
+        MARGIN = E2E_MARGIN
+    else:
+        assert_f32_rows_close(hid, hid_ref, "hidden")
+        assert_f32_rows_close(lg, lg_ref, "logits")
+        MARGIN = 1e-2
+    am = out["argmax"].cpu().numpy()[rows]
+    ok = margin >= MARGIN
+    assert np.array_equal(am[ok], am_ref[ok])
+    acc = out["accept_len"].cpu().numpy()
+    anc = out["next_anchor"].cpu().numpy()
+    r_acc, r_anc, _, _ = ref_accept(drafts_ref, targets[seqs])
+    compared = 0
+    for i, s in enumerate(seqs):
+        mg = margin.reshape(len(seqs), B)[i, 1:]
+        j = min(acc[s], r_acc[i])
+        if np.all(mg[:min(j + 1, B - 1)] >= MARGIN):
+            assert acc[s] == r_acc[i] and anc[s] == r_anc[i], (s, acc[s], r_acc[i])
+            compared += 1
+    print(f"  argmax compared {int(ok.sum())}/{ok.size}, acceptance compared {compared}/{len(seqs)},"
+          f" accept lens {acc[seqs].tolist()}", flush=True)
+    # GPU commit bookkeeping is consistent with its own accept lengths
+    offs = out["commit_offsets"].cpu().numpy()
+    assert np.array_equal(np.diff(offs), acc + 1)
+    return out
+
+
+def test_tiny_fp32_step():
+    wl = synth.tiny_fp32()
+    _step_case(wl, [64], [64], seqs=[0], uniform_targets=True)
+
+
+def test_small_bf16_step_cold():
+    wl = synth.small_bf16()
+    _step_case(wl, [512] * 4, [512] * 4, seqs=[0, 1, 2, 3])
+
+
+def test_small_bf16_step_warm():
+    wl = synth.small_bf16()
+    _step_case(wl, [512] * 4, [16] * 4, seqs=[0, 1, 2, 3], sub=1)
+
+
+def test_full_size_step_sampled():
+    """The benchmark's configuration: 8 x 2048 context, 16 new rows per sequence."""
+    wl = synth.drafter_full()
+    _step_case(wl, [2048] * 8, [16] * 8, seqs=[0, 7])
+    torch.cuda.empty_cache()
+
+
+def test_ragged_step_subset():
+    wl = synth.ragged_decode()
+    ctx = wl.ctx_lens[:6]
+    _step_case(wl, ctx, [16] * 6, seqs=[int(np.argmin(ctx)), int(np.argmax(ctx))], sub=2)
+    torch.cuda.empty_cache()

@@ -367,7 +367,7 @@ def test_gate_and_up_order_of_mlp():
     kv = context_kv(W, np.random.default_rng(9).standard_normal((3, d)), np.arange(3))
     toks = np.array([5, 6])
     out = block_forward(W, kv, toks)
-    h0 = W.tok_emb[toks]
+    h0 = np.asarray(W.tok_emb)[toks]
     v = h0 / np.sqrt(np.mean(h0 ** 2, axis=1, keepdims=True) + W.eps) * W.mlp_norm[0]
     h1 = h0 + v / (1 + np.exp(-v)) * (2 * v)
     want = h1 / np.sqrt(np.mean(h1 ** 2, axis=1, keepdims=True) + W.eps) * W.final_norm
