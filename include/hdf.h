@@ -144,12 +144,15 @@ typedef struct {
 hdf_status hdf_rope_table(float* out_host, int n_pos, int head_dim, double theta);
 
 /* KV cache, caller-owned, `dtype` elements:
- *   k  [n_layers][n_heads][kv_cap][head_dim]   keys after RoPE
- *   vt [n_layers][n_heads][head_dim][kv_cap]   values, transposed (positions fastest)
+ *   k  [n_layers][n_heads][kv_cap][head_dim]           keys after RoPE
+ *   vt [n_layers][n_heads][kv_cap/64][head_dim][64]    values in tiles of 64 positions,
+ *                                                      positions fastest in a tile
  * Context position i of sequence s lives at cache row kv_offsets[s] + i.  Every
  * kv_offsets[s] must be a multiple of 64 and kv_offsets[s+1] - kv_offsets[s] >= T_s
  * rounded up to a multiple of 64 (so 64-row tiles never leave a sequence's slot);
- * kv_cap >= kv_offsets[n_seq].  Rows past T_s inside a slot are never used. */
+ * kv_cap is a multiple of 64 and >= kv_offsets[n_seq].  Rows past T_s inside a slot
+ * are never used.  A 64-position tile of one head is thus 64*head_dim contiguous keys
+ * and 64*head_dim contiguous values: the attention streams both as whole tiles. */
 size_t hdf_kv_cache_bytes(const hdf_drafter* w, int64_t kv_cap); /* bytes of k (= of vt) */
 
 /* Workspace bytes hdf_draft_block needs for these sizes (0 on invalid arguments). */

@@ -5,9 +5,11 @@
 // fp32 softmax with online rescaling.
 //
 // Layouts (one layer): keys K[head][row][hd] (rows of a sequence contiguous),
-// values transposed Vt[head][hd][row] (rows fastest).  The context of sequence s
-// starts at cache row kv_offsets[s]; its block keys sit in a 64-row slot s of
-// separate block buffers of the same layout.
+// values in 64-row tiles Vt[head][row/64][hd][64] (rows fastest inside a tile), so
+// a 64-key tile of one head is 16 KB of contiguous keys plus 16 KB of contiguous
+// values.  The context of sequence s starts at cache row kv_offsets[s] (a multiple
+// of 64); its block keys sit in 64-row slot s of separate block buffers of the
+// same layout.
 //
 // bf16 kernel: grid (context chunk + 1 block chunk, head, sequence x 16-query
 // group), 4 waves.  A wave streams 64-key tiles and keeps its 16 queries' state
@@ -53,8 +55,7 @@ attn_bf16_kernel(AttnArgs a) {
   const int T = a.ctx_len[s];
 
   const bf16_t* kbase;
-  const bf16_t* vbase;
-  int64_t vstride;
+  const bf16_t* vbase;  // first value tile of the segment
   int k_lo, k_hi;
   if (chunk < a.n_chunks) {
     k_lo = chunk * a.chunk_len;
@@ -62,15 +63,12 @@ attn_bf16_kernel(AttnArgs a) {
     k_hi = min(T, k_lo + a.chunk_len);
     const int64_t row0 = a.kv_offsets[s];
     kbase = static_cast<const bf16_t*>(a.kc) + (int64_t(h) * a.cap + row0) * HD;
-    vbase = static_cast<const bf16_t*>(a.vtc) + int64_t(h) * HD * a.cap + row0;
-    vstride = a.cap;
+    vbase = static_cast<const bf16_t*>(a.vtc) + (int64_t(h) * (a.cap / 64) + row0 / 64) * HD * 64;
   } else {
     k_lo = 0;
     k_hi = a.B;
-    const int64_t row0 = int64_t(s) * 64;
-    kbase = static_cast<const bf16_t*>(a.kb) + (int64_t(h) * a.capb + row0) * HD;
-    vbase = static_cast<const bf16_t*>(a.vtb) + int64_t(h) * HD * a.capb + row0;
-    vstride = a.capb;
+    kbase = static_cast<const bf16_t*>(a.kb) + (int64_t(h) * a.capb + int64_t(s) * 64) * HD;
+    vbase = static_cast<const bf16_t*>(a.vtb) + (int64_t(h) * (a.capb / 64) + s) * HD * 64;
   }
 
   // Q^T operand: lane holds Q[query ql][32j + 8g .. +7].
@@ -102,13 +100,15 @@ attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
       for (int j = 0; j < NJ; ++j) kf[st][j] = __builtin_bit_cast(bf16x8_t, ld16(krow + 32 * j));
     }
-    // V^T operands: lane holds V^T[16dt + ql][t0 + 32ks + 8g .. +7].
+    // V^T operands: lane holds V^T[16dt + ql][t0 + 32ks + 8g .. +7], one 16-byte load
+    // from the tile of keys t0..t0+63.
+    const bf16_t* vtile = vbase + int64_t(t0 >> 6) * HD * 64;
     u32x4 vf[2][NDT];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
-        vf[ks][dt] = ld16(vbase + int64_t(16 * dt + ql) * vstride + t0 + 32 * ks + 8 * g);
+        vf[ks][dt] = ld16(vtile + (16 * dt + ql) * 64 + 32 * ks + 8 * g);
 
     float sv[4][4];
 #pragma unroll
@@ -225,41 +225,71 @@ attn_bf16_kernel(AttnArgs a) {
 }
 
 // Merge the chunk partials of one (sequence, head, 16-query group) -> O rows.
+// Phase 1 reads every chunk's (m, l), phase 2 turns them into per-chunk weights
+// exp2(m_c - M) / L, phase 3 forms each output quad from independent loads.
 template <typename T>
 __global__ void __launch_bounds__(kAttnThreads)
 attn_combine_kernel(AttnArgs a, T* __restrict__ out) {
+  extern __shared__ float cw[];  // [16][n_chunks + 1] weights, then [16][n_chunks + 1] m
   const int h = blockIdx.y;
   const int nqg = (a.B + 15) / 16;
   const int s = blockIdx.x / nqg;
   const int qg = blockIdx.x - s * nqg;
   const int T_s = a.ctx_len[s];
   const int nc = min(a.n_chunks, (T_s + a.chunk_len - 1) / a.chunk_len);
+  const int NC = a.n_chunks + 1;
+  float* cm = cw + 16 * NC;
   const int d = a.nh * a.hd;
-  for (int e = threadIdx.x; e < 16 * a.hd; e += kAttnThreads) {
-    const int qq = e / a.hd, dim = e - qq * a.hd;
+  const int64_t base = (int64_t(s) * a.nh + h) * NC;
+  // Phase 1: (m, l) of every used chunk (nc context chunks, then the block chunk).
+  for (int e = threadIdx.x; e < 16 * (nc + 1); e += kAttnThreads) {
+    const int qq = e / (nc + 1);
+    const int c = e - qq * (nc + 1);
+    const int cc = (c == nc) ? a.n_chunks : c;
+    const int64_t pi = (base + cc) * a.QB + qg * 16 + qq;
+    cm[qq * NC + c] = a.part_ml[pi * 2];
+    cw[qq * NC + c] = a.part_ml[pi * 2 + 1];
+  }
+  __syncthreads();
+  // Phase 2: per-query weights.
+  if (threadIdx.x < 16) {
+    const int qq = threadIdx.x;
+    float mm = -INFINITY;
+    for (int c = 0; c <= nc; ++c) mm = fmaxf(mm, cm[qq * NC + c]);
+    float l = 0.f;
+    for (int c = 0; c <= nc; ++c) {
+      const float f = (cm[qq * NC + c] == -INFINITY) ? 0.f : fast_exp2(cm[qq * NC + c] - mm);
+      cm[qq * NC + c] = f;
+      l += f * cw[qq * NC + c];
+    }
+    const float inv = 1.f / l;
+    for (int c = 0; c <= nc; ++c) cw[qq * NC + c] = cm[qq * NC + c] * inv;
+  }
+  __syncthreads();
+  // Phase 3: outputs, four consecutive dims per item.
+  const int quads = a.hd / 4;
+  for (int e = threadIdx.x; e < 16 * quads; e += kAttnThreads) {
+    const int qq = e / quads;
     const int q = qg * 16 + qq;
     if (q >= a.B) continue;
-    const int64_t base = (int64_t(s) * a.nh + h) * (a.n_chunks + 1);
-    float mm = -INFINITY;
+    const int i0 = (e - qq * quads) * 4;
+    float o[4] = {0.f, 0.f, 0.f, 0.f};
     for (int c = 0; c <= nc; ++c) {
       const int cc = (c == nc) ? a.n_chunks : c;
-      mm = fmaxf(mm, a.part_ml[((base + cc) * a.QB + q) * 2]);
+      const float wgt = cw[qq * NC + c];
+      const float4 v = *reinterpret_cast<const float4*>(
+          a.part_o + ((base + cc) * a.QB + q) * a.hd + i0);
+      o[0] = fmaf(wgt, v.x, o[0]);
+      o[1] = fmaf(wgt, v.y, o[1]);
+      o[2] = fmaf(wgt, v.z, o[2]);
+      o[3] = fmaf(wgt, v.w, o[3]);
     }
-    float o = 0.f, l = 0.f;
-    for (int c = 0; c <= nc; ++c) {
-      const int cc = (c == nc) ? a.n_chunks : c;
-      const int64_t pi = (base + cc) * a.QB + q;
-      const float mc = a.part_ml[pi * 2];
-      const float f = (mc == -INFINITY) ? 0.f : fast_exp2(mc - mm);
-      o += f * a.part_o[pi * a.hd + dim];
-      l += f * a.part_ml[pi * 2 + 1];
+    T* dst = out + (int64_t(s) * a.B + q) * d + int64_t(h) * a.hd + i0;
+    if constexpr (sizeof(T) == 2) {
+      *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf2(o[0], o[1]), pack_bf2(o[2], o[3]));
+    } else {
+      *reinterpret_cast<float4*>(dst) = make_float4(o[0], o[1], o[2], o[3]);
     }
-    const float v = o / l;
-    T* dst = out + (int64_t(s) * a.B + q) * d + int64_t(h) * a.hd + dim;
-    if constexpr (sizeof(T) == 2)
-      *dst = f2bf(v);
-    else
-      *dst = v;
   }
 }
 
@@ -280,20 +310,16 @@ __global__ void attn_f32_kernel(AttnArgs a, float* __restrict__ out) {
   float m = -INFINITY, l = 0.f;
   for (int seg = 0; seg < 2; ++seg) {
     const float* K;
-    const float* Vt;
-    int64_t vs;
+    const float* Vt;  // first value tile of the segment
     int n;
     if (seg == 0) {
       const int64_t row0 = a.kv_offsets[s];
       K = static_cast<const float*>(a.kc) + (int64_t(h) * a.cap + row0) * hd;
-      Vt = static_cast<const float*>(a.vtc) + int64_t(h) * hd * a.cap + row0;
-      vs = a.cap;
+      Vt = static_cast<const float*>(a.vtc) + (int64_t(h) * (a.cap / 64) + row0 / 64) * hd * 64;
       n = a.ctx_len[s];
     } else {
-      const int64_t row0 = int64_t(s) * 64;
-      K = static_cast<const float*>(a.kb) + (int64_t(h) * a.capb + row0) * hd;
-      Vt = static_cast<const float*>(a.vtb) + int64_t(h) * hd * a.capb + row0;
-      vs = a.capb;
+      K = static_cast<const float*>(a.kb) + (int64_t(h) * a.capb + int64_t(s) * 64) * hd;
+      Vt = static_cast<const float*>(a.vtb) + (int64_t(h) * (a.capb / 64) + s) * hd * 64;
       n = a.B;
     }
     for (int j = 0; j < n; ++j) {
@@ -305,7 +331,8 @@ __global__ void attn_f32_kernel(AttnArgs a, float* __restrict__ out) {
       const float p = expf(sc - mn);
       l = l * al + p;
 #pragma unroll
-      for (int i = 0; i < hd; ++i) o[i] = o[i] * al + p * Vt[int64_t(i) * vs + j];
+      for (int i = 0; i < hd; ++i)
+        o[i] = o[i] * al + p * Vt[(int64_t(j >> 6) * hd + i) * 64 + (j & 63)];
       m = mn;
     }
   }
@@ -333,8 +360,9 @@ hipError_t launch_attention(bool bf16, const AttnArgs& a, void* out, hipStream_t
     hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(kAttnThreads), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_combine_kernel<bf16_t>, dim3(a.n_seq * nqg, a.nh), dim3(kAttnThreads), 0,
-                     s, a, static_cast<bf16_t*>(out));
+  const size_t lds = size_t(2) * 16 * (a.n_chunks + 1) * sizeof(float);
+  hipLaunchKernelGGL(attn_combine_kernel<bf16_t>, dim3(a.n_seq * nqg, a.nh), dim3(kAttnThreads),
+                     lds, s, a, static_cast<bf16_t*>(out));
   return hipGetLastError();
 }
 

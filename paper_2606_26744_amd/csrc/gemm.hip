@@ -28,8 +28,7 @@
 namespace hdf {
 
 constexpr int kGemmThreads = 256;
-constexpr int kBK = 64;
-constexpr int kLDK = kBK + 8;  // padded LDS row (bf16 elements)
+constexpr int kBK = 64;        // K granularity of every GEMM (K % kBK == 0)
 
 __device__ __forceinline__ int remap_tile(int bid, int total) {
   // XCD-aware order: dispatch sends consecutive workgroups round-robin over the 8
@@ -93,13 +92,15 @@ __device__ __forceinline__ void argmax_epilogue(const float* Cs, int m0, int n0,
   }
 }
 
-template <int BM, int BN, int STAGES, int EPI>
+template <int BM, int BN, int BK, int STAGES, int EPI>
 __global__ void __launch_bounds__(kGemmThreads)
 gemm_bf16_kernel(GemmArgs p) {
   constexpr int WM = 2, WN = 2;
   constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
-  constexpr int A_CH = BM * kBK / 8 / kGemmThreads;  // 16-byte chunks per thread per K-tile
-  constexpr int B_CH = BN * kBK / 8 / kGemmThreads;
+  constexpr int kLDK = BK + 8;                       // padded LDS row (bf16 elements)
+  constexpr int CPR = BK / 8;                        // 16-byte chunks per row of a K-tile
+  constexpr int A_CH = BM * BK / 8 / kGemmThreads;  // 16-byte chunks per thread per K-tile
+  constexpr int B_CH = BN * BK / 8 / kGemmThreads;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   bf16_t* As = reinterpret_cast<bf16_t*>(smem);          // [2][BM][kLDK]
   bf16_t* Bs = As + 2 * BM * kLDK;                        // [2][BN][kLDK]
@@ -115,7 +116,7 @@ gemm_bf16_kernel(GemmArgs p) {
   const int n_tile = tile / mt, m_tile = tile % mt;
   const int m0 = m_tile * BM, n0 = n_tile * BN;
 
-  const int nk_all = p.K / kBK;
+  const int nk_all = p.K / BK;
   const int z = blockIdx.z;
   const int kt_begin = (nk_all * z) / gridDim.z;
   const int kt_end = (nk_all * (z + 1)) / gridDim.z;
@@ -126,32 +127,37 @@ gemm_bf16_kernel(GemmArgs p) {
 
   u32x4 ra[STAGES][A_CH], rb[STAGES][B_CH];
 
+  // Rows past M (or N) are clamped to the last valid row rather than predicated: they
+  // only feed accumulator rows/columns that are never stored, and unpredicated loads
+  // keep the compiler's outstanding-load counting exact, so the prefetched stages stay
+  // in flight across iterations.
+  // A wave instruction covers 64 / CPR rows x CPR*16 contiguous bytes of each row.
   auto gload = [&](int kt, u32x4* da, u32x4* db) {
-    const int64_t k = int64_t(kt_begin + kt) * kBK;
+    const int64_t k = int64_t(kt_begin + kt) * BK;
 #pragma unroll
     for (int i = 0; i < A_CH; ++i) {
       const int c = tid + i * kGemmThreads;
-      const int row = c >> 3, col = (c & 7) * 8;
-      da[i] = (m0 + row < p.M) ? ld16(A + int64_t(m0 + row) * p.lda + k + col) : u32x4{0, 0, 0, 0};
+      const int row = min(m0 + c / CPR, p.M - 1), col = (c % CPR) * 8;
+      da[i] = ld16(A + int64_t(row) * p.lda + k + col);
     }
 #pragma unroll
     for (int i = 0; i < B_CH; ++i) {
       const int c = tid + i * kGemmThreads;
-      const int row = c >> 3, col = (c & 7) * 8;
-      db[i] = (n0 + row < p.N) ? ld16(B + int64_t(n0 + row) * p.ldb + k + col) : u32x4{0, 0, 0, 0};
+      const int row = min(n0 + c / CPR, p.N - 1), col = (c % CPR) * 8;
+      db[i] = ld16(B + int64_t(row) * p.ldb + k + col);
     }
   };
   auto sstore = [&](const u32x4* da, const u32x4* db, int buf) {
 #pragma unroll
     for (int i = 0; i < A_CH; ++i) {
       const int c = tid + i * kGemmThreads;
-      const int row = c >> 3, col = (c & 7) * 8;
+      const int row = c / CPR, col = (c % CPR) * 8;
       *reinterpret_cast<u32x4*>(As + (buf * BM + row) * kLDK + col) = da[i];
     }
 #pragma unroll
     for (int i = 0; i < B_CH; ++i) {
       const int c = tid + i * kGemmThreads;
-      const int row = c >> 3, col = (c & 7) * 8;
+      const int row = c / CPR, col = (c % CPR) * 8;
       *reinterpret_cast<u32x4*>(Bs + (buf * BN + row) * kLDK + col) = db[i];
     }
   };
@@ -165,50 +171,51 @@ gemm_bf16_kernel(GemmArgs p) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   if (nk > 0) {
-#pragma unroll
-    for (int s = 0; s < STAGES; ++s)
-      if (s < nk) gload(s, ra[s], rb[s]);
-    sstore(ra[0], rb[0], 0);
-    __syncthreads();
-
     const int arow = wm * (BM / WM) + (lane & 31);
     const int brow = wn * (BN / WN) + (lane & 31);
     const int kof = 8 * (lane >> 5);
-
-    for (int kt0 = 0; kt0 < nk; kt0 += STAGES) {
+    auto compute = [&](int buf) {
+      const bf16_t* as = As + buf * BM * kLDK;
+      const bf16_t* bs = Bs + buf * BN * kLDK;
 #pragma unroll
-      for (int u = 0; u < STAGES; ++u) {
-        const int kt = kt0 + u;
-        if (kt < nk) {
-          // Refill the register stage that tile kt occupied (already in LDS).
-          if (kt + STAGES < nk) gload(kt + STAGES, ra[u], rb[u]);
-          const int buf = kt & 1;
-          const bf16_t* as = As + buf * BM * kLDK;
-          const bf16_t* bs = Bs + buf * BN * kLDK;
+      for (int ks = 0; ks < BK / 16; ++ks) {
+        bf16x8_t af[TM], bfr[TN];
 #pragma unroll
-          for (int ks = 0; ks < kBK / 16; ++ks) {
-            bf16x8_t af[TM], bfr[TN];
+        for (int i = 0; i < TM; ++i)
+          af[i] = *reinterpret_cast<const bf16x8_t*>(as + (arow + i * 32) * kLDK + ks * 16 + kof);
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-              af[i] = *reinterpret_cast<const bf16x8_t*>(as + (arow + i * 32) * kLDK + ks * 16 + kof);
+        for (int j = 0; j < TN; ++j)
+          bfr[j] = *reinterpret_cast<const bf16x8_t*>(bs + (brow + j * 32) * kLDK + ks * 16 + kof);
 #pragma unroll
-            for (int j = 0; j < TN; ++j)
-              bfr[j] = *reinterpret_cast<const bf16x8_t*>(bs + (brow + j * 32) * kLDK + ks * 16 + kof);
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-              for (int j = 0; j < TN; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-          }
-          if (kt + 1 < nk) {
-            constexpr int dummy = 0;
-            (void)dummy;
-            sstore(ra[(u + 1) % STAGES], rb[(u + 1) % STAGES], (kt + 1) & 1);
-          }
-          __syncthreads();
-        }
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
       }
+    };
+    // One K-tile step with ring slot u (a compile-time constant after unrolling):
+    // refill slot u with tile t+STAGES (tile t is already in LDS), compute tile t,
+    // move tile t+1 from its slot into the other LDS buffer, barrier.  Tile indices
+    // past the end are clamped to the last tile (an L2 hit, never used), so every
+    // load and store is unconditional.
+    auto step = [&](int t, int u) {
+      gload(min(t + STAGES, nk - 1), ra[u], rb[u]);
+      compute(t & 1);
+      sstore(ra[(u + 1) % STAGES], rb[(u + 1) % STAGES], (t + 1) & 1);
+      __syncthreads();
+    };
+#pragma unroll
+    for (int st = 0; st < STAGES; ++st) gload(min(st, nk - 1), ra[st], rb[st]);
+    sstore(ra[0], rb[0], 0);
+    __syncthreads();
+    int kt = 0;
+    for (; kt + STAGES <= nk; kt += STAGES) {
+#pragma unroll
+      for (int u = 0; u < STAGES; ++u) step(kt + u, u);
     }
+#pragma unroll
+    for (int u = 0; u < STAGES; ++u)
+      if (kt + u < nk) step(kt + u, u);
   }
 
   if constexpr (EPI == kEpiPartial) {
@@ -336,9 +343,9 @@ static hipError_t set_lds(K kern, size_t bytes) {
 
 template <int BM, int EPI>
 static hipError_t launch_bf16(const GemmArgs& a, int splits, hipStream_t s) {
-  constexpr int BN = 128, STAGES = 2;
-  auto kern = gemm_bf16_kernel<BM, BN, STAGES, EPI>;
-  const size_t main_lds = size_t(2) * (BM + BN) * kLDK * sizeof(bf16_t);
+  constexpr int BN = 128, BK = kBK, STAGES = 3;
+  auto kern = gemm_bf16_kernel<BM, BN, BK, STAGES, EPI>;
+  const size_t main_lds = size_t(2) * (BM + BN) * (BK + 8) * sizeof(bf16_t);
   const size_t epi_lds = (EPI == kEpiPartial) ? 0 : size_t(BM) * (BN + 4) * sizeof(float);
   const size_t lds = main_lds > epi_lds ? main_lds : epi_lds;
   hipError_t e = set_lds(kern, lds);
@@ -374,11 +381,13 @@ int gemm_pick_splits(bool bf16, int M, int N, int K) {
   const int BN = bf16 ? 128 : 64;
   const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
   const int nk = K / gemm_k_align(bf16);
-  const int target = device_cu_count() * 2;
+  // One wave of workgroups over the CUs; every split keeps at least 8 K-tiles and the
+  // fp32 partials (S * M * N * 4 bytes, read back once) stay small next to the weights.
+  const int target = device_cu_count();
   int s = (target + tiles - 1) / tiles;
-  const int max_s = nk / 4 > 1 ? nk / 4 : 1;  // at least 4 K-tiles per split
+  const int max_s = nk / 8 > 1 ? nk / 8 : 1;
   if (s > max_s) s = max_s;
-  if (s > 16) s = 16;
+  if (s > 8) s = 8;
   return s < 1 ? 1 : s;
 }
 

@@ -118,14 +118,22 @@ hc_reduce_kernel(const T* __restrict__ H, const T* __restrict__ Wg, const float*
 #pragma unroll
   for (int g = 0; g < MP; ++g) bias[g] = bg[g];
 
+  // Loads are never predicated: a token index past the end is clamped to the last
+  // token (its data is never used) and idle lanes read a valid column and zero it
+  // with a select.  Unpredicated loads keep the compiler's outstanding-load count
+  // exact, so the next token's loads stay in flight across the reduction.
+  int colc[SLOTS];
+#pragma unroll
+  for (int k = 0; k < SLOTS; ++k) colc[k] = act[k] ? col[k] : 0;
   auto load_token = [&](int64_t tt, u32x4* dst) {
+    const int64_t tc = tt < n_tok ? tt : n_tok - 1;
 #pragma unroll
     for (int j = 0; j < MP; ++j)
 #pragma unroll
-      for (int k = 0; k < SLOTS; ++k)
-        dst[j * SLOTS + k] = (act[k] && tt < n_tok)
-                                 ? ld_nt16(H + tt * row + int64_t(j) * d + col[k])
-                                 : u32x4{0, 0, 0, 0};
+      for (int k = 0; k < SLOTS; ++k) {
+        const u32x4 v = ld_nt16(H + tc * row + int64_t(j) * d + colc[k]);
+        dst[j * SLOTS + k] = act[k] ? v : u32x4{0, 0, 0, 0};
+      }
   };
 
   int64_t t = blockIdx.x;

@@ -122,28 +122,33 @@ embed_norm_kernel(const int32_t* __restrict__ tokens, const T* __restrict__ emb,
   }
 }
 
+// One 1024-thread workgroup per row: every thread owns at most two float4 groups, so
+// all split-K partial loads of a row are in flight together.
+constexpr int kResThreads = 1024;
+
 template <typename T>
-__global__ void __launch_bounds__(kRowThreads)
+__global__ void __launch_bounds__(kResThreads)
 residual_norm_kernel(const float* __restrict__ parts, int S, int64_t M,
                      const float* __restrict__ gamma, float eps, int d, float* __restrict__ h,
                      T* __restrict__ u) {
-  __shared__ float sh[kRowThreads / 64];
+  __shared__ float sh[kResThreads / 64];
   const int64_t r = blockIdx.x;
-  float v[kMaxGroups][4];
+  float v[2][4];
   float ss = 0.f;
 #pragma unroll
-  for (int g = 0; g < kMaxGroups; ++g) {
-    const int c = (g * kRowThreads + threadIdx.x) * 4;
+  for (int g = 0; g < 2; ++g) {
+    const int c = (g * kResThreads + threadIdx.x) * 4;
     if (c < d) {
-      float4 acc = *reinterpret_cast<const float4*>(parts + r * d + c);
+      float4 acc = *reinterpret_cast<const float4*>(h + r * d + c);
+      float4 p = *reinterpret_cast<const float4*>(parts + r * d + c);
+#pragma unroll 4
       for (int z = 1; z < S; ++z) {
         const float4 t = *reinterpret_cast<const float4*>(parts + (int64_t(z) * M + r) * d + c);
-        acc.x += t.x; acc.y += t.y; acc.z += t.z; acc.w += t.w;
+        p.x += t.x; p.y += t.y; p.z += t.z; p.w += t.w;
       }
-      float4 hv = *reinterpret_cast<const float4*>(h + r * d + c);
-      hv.x += acc.x; hv.y += acc.y; hv.z += acc.z; hv.w += acc.w;
-      *reinterpret_cast<float4*>(h + r * d + c) = hv;
-      v[g][0] = hv.x; v[g][1] = hv.y; v[g][2] = hv.z; v[g][3] = hv.w;
+      acc.x += p.x; acc.y += p.y; acc.z += p.z; acc.w += p.w;
+      *reinterpret_cast<float4*>(h + r * d + c) = acc;
+      v[g][0] = acc.x; v[g][1] = acc.y; v[g][2] = acc.z; v[g][3] = acc.w;
 #pragma unroll
       for (int j = 0; j < 4; ++j) ss = fmaf(v[g][j], v[g][j], ss);
     }
@@ -151,8 +156,8 @@ residual_norm_kernel(const float* __restrict__ parts, int S, int64_t M,
   ss = block_sum(ss, sh);
   const float rs = rsqrtf(ss / float(d) + eps);
 #pragma unroll
-  for (int g = 0; g < kMaxGroups; ++g) {
-    const int c = (g * kRowThreads + threadIdx.x) * 4;
+  for (int g = 0; g < 2; ++g) {
+    const int c = (g * kResThreads + threadIdx.x) * 4;
     if (c < d) {
       float o[4];
 #pragma unroll
@@ -197,75 +202,98 @@ __device__ __forceinline__ void row_dest(const QkvEpiArgs& a, int r, int& pos, i
   }
 }
 
-// Q and K columns: sum the split-K partials, rotate pairs (i, i+hd/2), store.
-// grid (M, number of rotated parts), one pair per thread iteration.
-template <typename T>
+// Projection epilogue of one tile of kQkvRows rows x one head: sums the split-K
+// partials, rotates (i, i+hd/2) pairs of Q and K at each row's position and stores
+// them row-major; V goes through LDS and is stored in 64-position tiles with
+// positions fastest ([head][row/64][hd][64]), so consecutive lanes store
+// consecutive positions.
+constexpr int kQkvRows = 16;
+
+template <typename T, int HD>
 __global__ void __launch_bounds__(kRowThreads)
-qk_rope_kernel(QkvEpiArgs a) {
-  const int r = blockIdx.x;
-  const int part = a.first_part + blockIdx.y;  // 0 = Q, 1 = K
+qkv_epilogue_kernel(QkvEpiArgs a) {
+  constexpr int HALF = HD / 2;
+  __shared__ float vt_tile[kQkvRows][HD + 1];
+  __shared__ int s_pos[kQkvRows], s_s[kQkvRows], s_k[kQkvRows];
+  __shared__ int64_t s_drow[kQkvRows];
+  const int r0 = blockIdx.x * kQkvRows;
+  const int h = blockIdx.y;
+  const int rows = min(kQkvRows, a.M - r0);
   const int ncol = (3 - a.first_part) * a.d;
-  const int half = a.hd / 2;
-  int pos, s, kslot;
-  int64_t drow;
-  row_dest(a, r, pos, drow, s, kslot);
-  const int64_t base = int64_t(r) * ncol + int64_t(part - a.first_part) * a.d;
-  for (int j = threadIdx.x; j < a.d / 2; j += kRowThreads) {
-    const int hh = j / half, i = j - hh * half;
-    const int64_t c1 = base + int64_t(hh) * a.hd + i;
-    float x1 = 0.f, x2 = 0.f;
-    for (int z = 0; z < a.S; ++z) {
-      const int64_t off = int64_t(z) * a.M * ncol;
-      x1 += a.parts[off + c1];
-      x2 += a.parts[off + c1 + half];
+  const int64_t zstride = int64_t(a.M) * ncol;
+  if (threadIdx.x < rows) {
+    int pos, s, k;
+    int64_t drow;
+    row_dest(a, r0 + threadIdx.x, pos, drow, s, k);
+    s_pos[threadIdx.x] = pos;
+    s_s[threadIdx.x] = s;
+    s_k[threadIdx.x] = k;
+    s_drow[threadIdx.x] = drow;
+  }
+  __syncthreads();
+  const int nrot = 2 - a.first_part;  // Q and K, or K only
+  // Rotated parts: items (row, part, quad of 4 consecutive i < HALF).
+  constexpr int QUADS = HALF / 4;
+  for (int e = threadIdx.x; e < rows * nrot * QUADS; e += kRowThreads) {
+    const int rr = e / (nrot * QUADS);
+    const int rem = e - rr * nrot * QUADS;
+    const int pp = rem / QUADS;
+    const int i0 = (rem - pp * QUADS) * 4;
+    const int part = a.first_part + pp;
+    const int64_t c = int64_t(r0 + rr) * ncol + int64_t(pp) * a.d + int64_t(h) * HD + i0;
+    float4 x1 = *reinterpret_cast<const float4*>(a.parts + c);
+    float4 x2 = *reinterpret_cast<const float4*>(a.parts + c + HALF);
+    for (int z = 1; z < a.S; ++z) {
+      const float4 t1 = *reinterpret_cast<const float4*>(a.parts + z * zstride + c);
+      const float4 t2 = *reinterpret_cast<const float4*>(a.parts + z * zstride + c + HALF);
+      x1.x += t1.x; x1.y += t1.y; x1.z += t1.z; x1.w += t1.w;
+      x2.x += t2.x; x2.y += t2.y; x2.z += t2.z; x2.w += t2.w;
     }
-    float y1 = x1, y2 = x2;
+    float y1[4] = {x1.x, x1.y, x1.z, x1.w}, y2[4] = {x2.x, x2.y, x2.z, x2.w};
     if (a.rope_cs != nullptr) {
-      const float2 cs = *reinterpret_cast<const float2*>(a.rope_cs + (int64_t(pos) * half + i) * 2);
-      y1 = x1 * cs.x - x2 * cs.y;
-      y2 = x2 * cs.x + x1 * cs.y;
+      const float* cs = a.rope_cs + (int64_t(s_pos[rr]) * HALF + i0) * 2;
+      const float4 cs01 = *reinterpret_cast<const float4*>(cs);
+      const float4 cs23 = *reinterpret_cast<const float4*>(cs + 4);
+      const float cv[4] = {cs01.x, cs01.z, cs23.x, cs23.z};
+      const float sv[4] = {cs01.y, cs01.w, cs23.y, cs23.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float u1 = y1[j], u2 = y2[j];
+        y1[j] = u1 * cv[j] - u2 * sv[j];
+        y2[j] = u2 * cv[j] + u1 * sv[j];
+      }
     }
     T* dst;
     if (part == 0)
-      dst = static_cast<T*>(a.q) + ((int64_t(s) * a.nh + hh) * a.B + kslot) * a.hd;
+      dst = static_cast<T*>(a.q) + ((int64_t(s_s[rr]) * a.nh + h) * a.B + s_k[rr]) * HD;
     else
-      dst = static_cast<T*>(a.k) + (int64_t(hh) * a.cap + drow) * a.hd;
-    store1<T>(dst + i, y1);
-    store1<T>(dst + i + half, y2);
+      dst = static_cast<T*>(a.k) + (int64_t(h) * a.cap + s_drow[rr]) * HD;
+    store4<T>(dst + i0, y1);
+    store4<T>(dst + i0 + HALF, y2);
   }
-}
-
-// V columns: sum partials and write transposed (positions fastest) through an LDS
-// tile of 64 rows x 64 columns.
-template <typename T>
-__global__ void __launch_bounds__(kRowThreads)
-v_transpose_kernel(QkvEpiArgs a) {
-  __shared__ float tile[64][65];
-  const int r0 = blockIdx.x * 64;
-  const int c0 = blockIdx.y * 64;
-  const int ncol = (3 - a.first_part) * a.d;
-  const int64_t vcol = int64_t(2 - a.first_part) * a.d;
-  for (int e = threadIdx.x; e < 64 * 64; e += kRowThreads) {
-    const int rr = e >> 6, cc = e & 63;
-    float x = 0.f;
-    if (r0 + rr < a.M) {
-      for (int z = 0; z < a.S; ++z)
-        x += a.parts[(int64_t(z) * a.M + r0 + rr) * ncol + vcol + c0 + cc];
+  // V part -> LDS.
+  const int64_t vcol = int64_t(2 - a.first_part) * a.d + int64_t(h) * HD;
+  for (int e = threadIdx.x; e < rows * (HD / 4); e += kRowThreads) {
+    const int rr = e / (HD / 4);
+    const int i0 = (e - rr * (HD / 4)) * 4;
+    const int64_t c = int64_t(r0 + rr) * ncol + vcol + i0;
+    float4 x = *reinterpret_cast<const float4*>(a.parts + c);
+    for (int z = 1; z < a.S; ++z) {
+      const float4 t = *reinterpret_cast<const float4*>(a.parts + z * zstride + c);
+      x.x += t.x; x.y += t.y; x.z += t.z; x.w += t.w;
     }
-    tile[rr][cc] = x;
+    vt_tile[rr][i0 + 0] = x.x;
+    vt_tile[rr][i0 + 1] = x.y;
+    vt_tile[rr][i0 + 2] = x.z;
+    vt_tile[rr][i0 + 3] = x.w;
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < 64 * 64; e += kRowThreads) {
-    const int cc = e >> 6, rr = e & 63;
-    const int r = r0 + rr;
-    if (r >= a.M) continue;
-    int pos, s, kslot;
-    int64_t drow;
-    row_dest(a, r, pos, drow, s, kslot);
-    const int col = c0 + cc;
-    const int hh = col / a.hd, i = col - hh * a.hd;
-    T* dst = static_cast<T*>(a.vt) + (int64_t(hh) * a.hd + i) * a.cap + drow;
-    store1<T>(dst, tile[rr][cc]);
+  T* vt = static_cast<T*>(a.vt) + int64_t(h) * (a.cap / 64) * HD * 64;
+  for (int e = threadIdx.x; e < rows * HD; e += kRowThreads) {
+    const int i = e / rows;
+    const int rr = e - i * rows;
+    const int64_t drow = s_drow[rr];
+    store1<T>(vt + ((drow >> 6) * HD + i) * 64 + (drow & 63), vt_tile[rr][i]);
   }
 }
 
@@ -334,24 +362,27 @@ hipError_t launch_residual_norm(bool bf16, const float* parts, int S, const floa
                                 int64_t rows, int d, float* h, void* u, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (bf16)
-    hipLaunchKernelGGL(residual_norm_kernel<bf16_t>, dim3(unsigned(rows)), dim3(kRowThreads), 0, s,
+    hipLaunchKernelGGL(residual_norm_kernel<bf16_t>, dim3(unsigned(rows)), dim3(kResThreads), 0, s,
                        parts, S, rows, gamma, eps, d, h, static_cast<bf16_t*>(u));
   else
-    hipLaunchKernelGGL(residual_norm_kernel<float>, dim3(unsigned(rows)), dim3(kRowThreads), 0, s,
+    hipLaunchKernelGGL(residual_norm_kernel<float>, dim3(unsigned(rows)), dim3(kResThreads), 0, s,
                        parts, S, rows, gamma, eps, d, h, static_cast<float*>(u));
   return hipGetLastError();
 }
 
 hipError_t launch_qkv_epilogue(bool bf16, const QkvEpiArgs& a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  const dim3 g1(unsigned(a.M), unsigned(2 - a.first_part));
-  const dim3 g2(unsigned((a.M + 63) / 64), unsigned(a.d / 64));
+  const dim3 grid(unsigned((a.M + kQkvRows - 1) / kQkvRows), unsigned(a.nh));
   if (bf16) {
-    hipLaunchKernelGGL(qk_rope_kernel<bf16_t>, g1, dim3(kRowThreads), 0, s, a);
-    hipLaunchKernelGGL(v_transpose_kernel<bf16_t>, g2, dim3(kRowThreads), 0, s, a);
+    if (a.hd == 128)
+      hipLaunchKernelGGL((qkv_epilogue_kernel<bf16_t, 128>), grid, dim3(kRowThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((qkv_epilogue_kernel<bf16_t, 64>), grid, dim3(kRowThreads), 0, s, a);
   } else {
-    hipLaunchKernelGGL(qk_rope_kernel<float>, g1, dim3(kRowThreads), 0, s, a);
-    hipLaunchKernelGGL(v_transpose_kernel<float>, g2, dim3(kRowThreads), 0, s, a);
+    if (a.hd == 128)
+      hipLaunchKernelGGL((qkv_epilogue_kernel<float, 128>), grid, dim3(kRowThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((qkv_epilogue_kernel<float, 64>), grid, dim3(kRowThreads), 0, s, a);
   }
   return hipGetLastError();
 }

@@ -242,8 +242,12 @@ class DrafterHandle:
         return int(lib().hdf_draft_block_workspace(ctypes.byref(self.s), n_seq, B, n_new, max_ctx))
 
     def alloc_kv(self, kv_cap: int, device="cuda"):
+        """KV cache tensors in the library's layout: k [L][nh][cap][hd], vt
+        [L][nh][cap/64][hd][64] (values in 64-position tiles, positions fastest)."""
+        if kv_cap % 64:
+            raise ValueError("kv_cap must be a multiple of 64")
         shape_k = (self.L, self.nh, kv_cap, self.hd)
-        shape_vt = (self.L, self.nh, self.hd, kv_cap)
+        shape_vt = (self.L, self.nh, kv_cap // 64, self.hd, 64)
         return (torch.zeros(shape_k, dtype=self.torch_dtype, device=device),
                 torch.zeros(shape_vt, dtype=self.torch_dtype, device=device))
 
@@ -266,6 +270,35 @@ class DrafterHandle:
                                      _ptr(kv_k), _ptr(kv_vt), kv_cap, _ptr(tokens), _ptr(hidden),
                                      _ptr(ws), ws.numel(), _stream(stream)))
         return hidden
+
+
+def write_kv_rows(kv_k: torch.Tensor, kv_vt: torch.Tensor, layer: int, row0: int,
+                  k_rows: torch.Tensor, v_rows: torch.Tensor):
+    """Copies keys/values of consecutive positions [n, nh*hd] into cache rows row0..row0+n-1
+    (row0 a multiple of 64) of one layer.  Layout conversion only."""
+    n = k_rows.shape[0]
+    if n == 0:
+        return
+    _, nh, _, hd = kv_k.shape
+    if row0 % 64:
+        raise ValueError("row0 must be a multiple of 64")
+    kv_k[layer, :, row0:row0 + n, :] = k_rows.view(n, nh, hd).permute(1, 0, 2)
+    n64 = (n + 63) // 64
+    vp = torch.zeros((n64 * 64, nh, hd), dtype=v_rows.dtype, device=v_rows.device)
+    vp[:n] = v_rows.view(n, nh, hd)
+    t0 = row0 // 64
+    kv_vt[layer, :, t0:t0 + n64] = vp.view(n64, 64, nh, hd).permute(2, 0, 3, 1)
+
+
+def read_kv_rows(kv_k: torch.Tensor, kv_vt: torch.Tensor, layer: int, row0: int, n: int):
+    """Keys/values of cache rows row0..row0+n-1 of one layer as [n, nh*hd] tensors."""
+    _, nh, _, hd = kv_k.shape
+    k = kv_k[layer, :, row0:row0 + n, :].permute(1, 0, 2).reshape(n, nh * hd)
+    t_lo, t_hi = row0 // 64, (row0 + n + 63) // 64
+    vt = kv_vt[layer, :, t_lo:t_hi]                       # [nh][tiles][hd][64]
+    v = vt.permute(1, 3, 0, 2).reshape((t_hi - t_lo) * 64, nh * hd)
+    off = row0 - t_lo * 64
+    return k.contiguous(), v[off:off + n].contiguous()
 
 
 def kv_slot_offsets(ctx_lens: Sequence[int]) -> list:

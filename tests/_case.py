@@ -47,9 +47,7 @@ class DraftCase:
             for l in range(L):
                 if t0 > 0:
                     k, v = synth.kv_prefix(wl, t0, l, device=dev, sub=sub * 1000 + s)
-                    o = offs[s]
-                    self.kv_k[l, :, o:o + t0, :] = k.view(t0, nh, hd).permute(1, 0, 2)
-                    self.kv_vt[l, :, :, o:o + t0] = v.view(t0, nh, hd).permute(1, 2, 0)
+                    hdf.write_kv_rows(self.kv_k, self.kv_vt, l, offs[s], k, v)
                     per_layer.append((bits(k), bits(v)))
                 else:
                     per_layer.append((np.zeros((0, dr.d)), np.zeros((0, dr.d))))

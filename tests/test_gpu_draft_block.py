@@ -7,6 +7,7 @@ import torch
 import synth
 from oracle.drafter import context_kv, draft_block as ref_draft
 from oracle.numerics import as_f64
+from paper_2606_26744_amd import hdf
 from tests._case import DraftCase, bits
 from tests._tol import assert_bf16_state_close, assert_f32_rows_close
 
@@ -39,8 +40,8 @@ def _compare(case, seqs=None, check_cache=True):
                 continue
             kv = context_kv(W, as_f64(case.y_rows(s)), np.arange(T - n, T))
             for l in range(dr.n_layers):
-                k = case.kv_k[l, :, offs[s] + T - n:offs[s] + T, :].permute(1, 0, 2).reshape(n, -1)
-                v = case.kv_vt[l, :, :, offs[s] + T - n:offs[s] + T].permute(2, 0, 1).reshape(n, -1)
+                kk, vv = hdf.read_kv_rows(case.kv_k, case.kv_vt, l, offs[s], T)
+                k, v = kk[T - n:], vv[T - n:]
                 if case.wl.dtype == "bf16":
                     assert_bf16_state_close(as_f64(bits(k.contiguous())), kv[l][0], "cache K")
                     assert_bf16_state_close(as_f64(bits(v.contiguous())), kv[l][1], "cache V")
