@@ -93,6 +93,27 @@ hdf_status hdf_hc_reduce(const void* H, const void* W_g, const float* b_g, int64
                          void* Y, float* alpha, hdf_stream_t stream);
 
 /* ------------------------------------------------------------------------------
+ * Weight layout of every projection and of the LM head.
+ *
+ * A weight W[N][K] (N outputs, K inputs; PyTorch's [out][in]) is passed in the
+ * MFMA-packed layout: element (n, k) sits at
+ *     (((n/128) * (K/16) + k/16) * 4 + (n%128)/32) * 512
+ *       + ((n%32) + 32*((k%16)/8)) * 8  +  k%8
+ * so each block of 32 rows x 16 columns is 512 contiguous elements in the order the
+ * 64 lanes of a wave hold a matrix-core operand, the four 32-row blocks of a 128-row
+ * group sit side by side for every 16 columns, and the groups follow each other
+ * along K.  Rows are padded with zeros to a multiple of 128.  Pack once when the
+ * weights are loaded.  Sub-matrices of whole 128-row groups are plain offsets into a
+ * packed matrix (rows r..r+n of W start at element r*K when r%128 == 0).
+ * ----------------------------------------------------------------------------*/
+/* Bytes of the packed copy of an N x K weight (0 on invalid arguments). */
+size_t hdf_packed_weight_bytes(int N, int K, hdf_dtype dtype);
+/* W [N][K] row-major (device) -> W_packed (device, hdf_packed_weight_bytes bytes).
+ * Limits: N >= 1, K a positive multiple of 16; W_packed must not overlap W. */
+hdf_status hdf_pack_weight(const void* W, void* W_packed, int N, int K, hdf_dtype dtype,
+                           hdf_stream_t stream);
+
+/* ------------------------------------------------------------------------------
  * 2. One-pass block drafter (Sec. 1, Sec. 2.1, Sec. 2.3).
  *
  * Each sequence s has a context of T_s positions whose reduced states were
@@ -124,9 +145,10 @@ typedef struct {
   int n_layers, d, n_heads, head_dim, d_ff, vocab;
   hdf_dtype dtype;
   float eps;                     /* RMSNorm epsilon for every norm (> 0)                */
-  const void* tok_emb;           /* [vocab][d]                                          */
+  const void* tok_emb;           /* [vocab][d] row-major (rows are gathered by token id) */
   const float* ctx_norm;         /* [d] or NULL (all ones)                              */
   const float* const* attn_norm; /* host array [n_layers] of device [d] (entries NULL = ones) */
+  /* Projection weights, each packed (hdf_pack_weight):                                */
   const void* const* w_qkv;      /* host array [n_layers] of device [3d][d]: Wq;Wk;Wv rows */
   const void* const* w_o;        /* host array [n_layers] of device [d][d]              */
   const float* const* mlp_norm;  /* host array [n_layers] of device [d] (NULL = ones)   */
@@ -177,7 +199,7 @@ size_t hdf_draft_block_workspace(const hdf_drafter* w, int n_seq, int B, int64_t
  * hidden      [n_seq*B][d] dtype (out): final-normed block states, row s*B + k
  * ws, ws_bytes  workspace of at least hdf_draft_block_workspace(...) bytes, 256-byte
  *             aligned; its contents on entry do not matter.
- * Limits: head_dim in {64, 128}; n_heads * head_dim == d; d % 64 == 0;
+ * Limits: head_dim in {64, 128}; n_heads * head_dim == d; d % 128 == 0;
  *         d_ff % 64 == 0; max_ctx + B <= rope_max_pos when rope_cs is given. */
 hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t* ctx_len,
                            int max_ctx, const void* y_new, const int32_t* new_offsets,
@@ -194,7 +216,7 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
  * ----------------------------------------------------------------------------*/
 size_t hdf_lm_head_workspace(int64_t M, int vocab);
 
-/* hidden    [M][d] dtype; W_lm [vocab][d] dtype
+/* hidden    [M][d] dtype; W_lm [vocab][d] dtype, packed (hdf_pack_weight)
  * argmax    [M] int32 (out)
  * max_logit [M] fp32 (out, may be NULL)
  * logits    [M][vocab] fp32 (out, may be NULL; for tests)

@@ -70,8 +70,8 @@ hdf_status validate_drafter(const hdf_drafter* w) {
     return fail(HDF_E_INVALID, "drafter: n_heads * head_dim != d");
   if (w->head_dim != 64 && w->head_dim != 128)
     return fail(HDF_E_UNSUPPORTED, "drafter: head_dim %d not in {64, 128}", w->head_dim);
-  if (w->d % 64 != 0 || w->d > 8192)
-    return fail(HDF_E_UNSUPPORTED, "drafter: d=%d must be a multiple of 64 up to 8192", w->d);
+  if (w->d % 128 != 0 || w->d > 8192)
+    return fail(HDF_E_UNSUPPORTED, "drafter: d=%d must be a multiple of 128 up to 8192", w->d);
   if (w->d_ff % 64 != 0) return fail(HDF_E_UNSUPPORTED, "drafter: d_ff %% 64 != 0");
   if (!(w->eps > 0.f)) return fail(HDF_E_INVALID, "drafter: eps must be > 0");
   if (w->tok_emb == nullptr || w->w_qkv == nullptr || w->w_o == nullptr ||
@@ -299,9 +299,10 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
       HDF_TRY(hdf::launch_row_norm(bf, static_cast<const char*>(y_new) + r0 * d * el, w->ctx_norm,
                                    w->eps, rows, d, cbuf, s));
       for (int l = 0; l < L; ++l) {
+        // Rows d..3d-1 (W_k; W_v) of the packed W_qkv: d/128 whole row groups in.
         const char* wkv = static_cast<const char*>(w->w_qkv[l]) + size_t(d) * d * el;
         const int S = hdf::gemm_pick_splits(bf, rows, 2 * d, d);
-        HDF_TRY(hdf::launch_gemm_partial(bf, cbuf, d, wkv, d, rows, 2 * d, d, S, parts, s));
+        HDF_TRY(hdf::launch_gemm_partial(bf, cbuf, d, wkv, rows, 2 * d, d, S, parts, s));
         hdf::QkvEpiArgs ea{};
         ea.parts = parts; ea.S = S; ea.M = rows; ea.first_part = 1;
         ea.d = d; ea.nh = nh; ea.hd = hd; ea.B = B;
@@ -322,7 +323,7 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
   for (int l = 0; l < L; ++l) {
     // Q, K_b, V_b with RoPE at T_s + k.
     const int Sq = hdf::gemm_pick_splits(bf, M, 3 * d, d);
-    HDF_TRY(hdf::launch_gemm_partial(bf, u, d, w->w_qkv[l], d, M, 3 * d, d, Sq, parts, s));
+    HDF_TRY(hdf::launch_gemm_partial(bf, u, d, w->w_qkv[l], M, 3 * d, d, Sq, parts, s));
     hdf::QkvEpiArgs ea{};
     ea.parts = parts; ea.S = Sq; ea.M = M; ea.first_part = 0;
     ea.d = d; ea.nh = nh; ea.hd = hd; ea.B = B;
@@ -344,20 +345,39 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
 
     // h += O Wo^T; u = RMSNorm(h) * mlp_norm.
     const int So = hdf::gemm_pick_splits(bf, M, d, d);
-    HDF_TRY(hdf::launch_gemm_partial(bf, attn, d, w->w_o[l], d, M, d, d, So, parts, s));
+    HDF_TRY(hdf::launch_gemm_partial(bf, attn, d, w->w_o[l], M, d, d, So, parts, s));
     HDF_TRY(hdf::launch_residual_norm(bf, parts, So, w->mlp_norm[l], w->eps, M, d, h, u, s));
 
     // act = SiLU(u Wg^T) * (u Wu^T); h += act Wd^T; next norm.
     const int Sg = hdf::gemm_pick_splits(bf, M, 2 * F, d);
-    HDF_TRY(hdf::launch_gemm_partial(bf, u, d, w->w_gate_up[l], d, M, 2 * F, d, Sg, parts, s));
+    HDF_TRY(hdf::launch_gemm_partial(bf, u, d, w->w_gate_up[l], M, 2 * F, d, Sg, parts, s));
     HDF_TRY(hdf::launch_silu_epilogue(bf, parts, Sg, M, F, act, s));
     const int Sd = hdf::gemm_pick_splits(bf, M, d, F);
-    HDF_TRY(hdf::launch_gemm_partial(bf, act, F, w->w_down[l], F, M, d, F, Sd, parts, s));
+    HDF_TRY(hdf::launch_gemm_partial(bf, act, F, w->w_down[l], M, d, F, Sd, parts, s));
     const bool last = (l + 1 == L);
     HDF_TRY(hdf::launch_residual_norm(bf, parts, Sd, last ? w->final_norm : w->attn_norm[l + 1],
                                       w->eps, M, d, h, last ? hidden : u, s));
   }
 #undef HDF_TRY
+  return ok();
+}
+
+size_t hdf_packed_weight_bytes(int N, int K, hdf_dtype dtype) {
+  if (N < 1 || K < 16 || K % 16 != 0 || (dtype != HDF_F32 && dtype != HDF_BF16)) return 0;
+  return hdf::packed_weight_elems(N, K) * (dtype == HDF_BF16 ? 2 : 4);
+}
+
+hdf_status hdf_pack_weight(const void* W, void* W_packed, int N, int K, hdf_dtype dtype,
+                           hdf_stream_t stream) {
+  if (dtype != HDF_F32 && dtype != HDF_BF16) return fail(HDF_E_INVALID, "pack_weight: bad dtype");
+  if (N < 1 || K < 16 || K % 16 != 0)
+    return fail(HDF_E_INVALID, "pack_weight: N=%d K=%d (need N >= 1, K a positive multiple of 16)",
+                N, K);
+  if (W == nullptr || W_packed == nullptr) return fail(HDF_E_INVALID, "pack_weight: null pointer");
+  if (W == W_packed) return fail(HDF_E_INVALID, "pack_weight: in-place packing is not supported");
+  hipError_t e = hdf::launch_pack_weight(dtype == HDF_BF16, W, W_packed, N, K,
+                                         reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "pack_weight launch");
   return ok();
 }
 

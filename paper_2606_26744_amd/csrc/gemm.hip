@@ -1,114 +1,79 @@
-// Dense contractions of the drafter step: C[M][N] = A[M][K] . B[N][K]^T with
-// fp32 accumulation.  Both operands are K-contiguous (the [out][in] layout of
-// every projection and of the LM head), which is the natural operand layout of
-// the CDNA matrix cores.
+// Dense contractions of the drafter step: C[M][N] = A[M][K] . W[N][K]^T with fp32
+// accumulation.  A (activations) is row-major; W (weights) is stored in the
+// MFMA-packed layout of hdf_pack_weight:
+//   element (n, k) at (((n/128)*(K/16) + k/16)*4 + (n%128)/32)*512
+//                     + ((n%32) + 32*((k%16)/8))*8 + k%8
+// i.e. every block of 32 rows x 16 k is 512 elements laid out in exactly the order
+// the 64 lanes of a wave hold the B operand of v_mfma_f32_32x32x16_bf16 (lane l: row
+// l%32, k 8*(l/32)..+7), and the four 32-row blocks of a 128-row group sit side by
+// side for every 16 k.  A wave streams its weights straight from HBM into registers
+// with one contiguous 1 KB load per instruction, the four waves of a workgroup read
+// one contiguous 16 KB run per 64-k step, and no weight byte passes through LDS.
 //
-// bf16: v_mfma_f32_32x32x16_bf16 on 128x128 (or 64x128) tiles, BK = 64, four
-// waves of 64 lanes in a 2x2 grid.  Global->LDS staging goes through registers
-// with STAGES K-tiles in flight per workgroup (the weight stream of the skinny
-// GEMMs is HBM-bound, so bytes in flight per CU set the speed); the LDS tiles are
-// double-buffered and padded by 16 bytes per row so the 16-byte operand reads of
-// 32 consecutive rows hit distinct banks.  Split-K runs over gridDim.z.
-// Tiles are handed out so that workgroups sharing a B tile (the weights) run on
-// the same XCD back to back and meet in that XCD's L2.
+// bf16 weight-streaming kernel: 4 waves, each owning 32 output columns and all BM
+// rows (BM = 128, or 64 when M <= 64) of a 128-column tile.  The activation slice
+// (BM x 64) is shared through a double-buffered, padded LDS tile.  A ring of
+// STAGES K-steps of weights is in flight per wave; activations are fetched one step
+// further ahead than weights because memory counters complete in issue order.
+// Split-K runs over gridDim.z; tiles are ordered so that the M-tiles of one weight
+// column block run on the same XCD back to back (its L2 serves the re-reads).
 //
 // Epilogues:
 //   PARTIAL  fp32 C (or split-K partial z at C + z*M*N) straight from registers
-//   ARGMAX   LM head: the tile is staged in LDS, each row's (max, lowest index)
-//            is folded into a packed 64-bit key with one atomicMax per row and
-//            tile; the logits are stored only when asked for
+//   ARGMAX   LM head: per row (max, lowest index) reduced across lanes, then across
+//            the four waves in LDS, folded into a packed 64-bit key with one atomicMax
+//            per row and tile; the logits are stored only when asked for
 //
-// fp32 (small correctness-size workloads): a plain LDS-tiled VALU kernel with
-// the same epilogues.
-#include <atomic>
-
+// fp32 (small correctness-size workloads): a plain LDS-tiled VALU kernel reading the
+// same packed weight layout, with the same epilogues.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace hdf {
 
 constexpr int kGemmThreads = 256;
-constexpr int kBK = 64;        // K granularity of every GEMM (K % kBK == 0)
+constexpr int kBK = 64;        // K granularity of the bf16 kernel (K % kBK == 0)
+
+__host__ __device__ __forceinline__ int64_t packed_index(int64_t n, int64_t k, int64_t K) {
+  return (((n >> 7) * (K >> 4) + (k >> 4)) * 4 + ((n >> 5) & 3)) * 512 +
+         ((n & 31) + 32 * ((k & 15) >> 3)) * 8 + (k & 7);
+}
 
 __device__ __forceinline__ int remap_tile(int bid, int total) {
   // XCD-aware order: dispatch sends consecutive workgroups round-robin over the 8
-  // XCDs; give each XCD a contiguous run of tile ids (tiles of one B column block
-  // are consecutive ids).
+  // XCDs; give each XCD a contiguous run of tile ids (the M-tiles of one weight
+  // column block are consecutive ids).
   const int per = total >> 3;
   if (bid < (per << 3)) return (bid & 7) * per + (bid >> 3);
   return bid;
 }
 
-// Row-wise (max, lowest index) of an fp32 tile staged in LDS, folded into keys[].
-template <int BM, int BN, int LDC>
-__device__ __forceinline__ void argmax_epilogue(const float* Cs, int m0, int n0, int M, int N,
-                                                unsigned long long* keys, float* logits) {
-  constexpr int TPR = kGemmThreads / BM;  // threads per row (2 or 4)
-  constexpr int CPT = BN / TPR;           // columns per thread
-  const int tid = threadIdx.x;
-  const int r = tid / TPR;
-  const int part = tid % TPR;
-  const int row = m0 + r;
-  float best = -INFINITY;
-  int bcol = 0x7FFFFFFF;
-  if (row < M) {
-    const int c0 = part * CPT;
-#pragma unroll 4
-    for (int c = 0; c < CPT; ++c) {
-      const int col = n0 + c0 + c;
-      const float v = Cs[r * LDC + c0 + c];
-      if (col < N && v > best) {
-        best = v;
-        bcol = col;
-      }
-    }
-  }
-#pragma unroll
-  for (int o = 1; o < TPR; o <<= 1) {
-    const float ov = __shfl_xor(best, o, kWave);
-    const int oc = __shfl_xor(bcol, o, kWave);
-    if (ov > best || (ov == best && oc < bcol)) {
-      best = ov;
-      bcol = oc;
-    }
-  }
-  if (part == 0 && row < M && bcol != 0x7FFFFFFF) {
-    const unsigned long long key =
-        (static_cast<unsigned long long>(f32_order_key(best)) << 32) |
-        static_cast<unsigned long long>(0xFFFFFFFFu - static_cast<uint32_t>(bcol));
-    atomicMax(keys + row, key);
-  }
-  if (logits != nullptr) {
-    // Coalesced copy of the tile: each thread moves 4 consecutive columns.
-    for (int i = tid * 4; i < BM * BN; i += kGemmThreads * 4) {
-      const int rr = i / BN, cc = i % BN;
-      const int grow = m0 + rr, gcol = n0 + cc;
-      if (grow >= M) continue;
-      float* dst = logits + int64_t(grow) * N + gcol;
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (gcol + j < N) dst[j] = Cs[rr * LDC + cc + j];
-    }
-  }
+__device__ __forceinline__ unsigned long long argmax_key(float v, int col) {
+  return (static_cast<unsigned long long>(f32_order_key(v)) << 32) |
+         static_cast<unsigned long long>(0xFFFFFFFFu - static_cast<uint32_t>(col));
 }
 
-template <int BM, int BN, int BK, int STAGES, int EPI>
-__global__ void __launch_bounds__(kGemmThreads)
+template <int BM, int NW, int STAGES, int EPI>
+__global__ void __launch_bounds__(NW * 64)
 gemm_bf16_kernel(GemmArgs p) {
-  constexpr int WM = 2, WN = 2;
-  constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
-  constexpr int kLDK = BK + 8;                       // padded LDS row (bf16 elements)
-  constexpr int CPR = BK / 8;                        // 16-byte chunks per row of a K-tile
-  constexpr int A_CH = BM * BK / 8 / kGemmThreads;  // 16-byte chunks per thread per K-tile
-  constexpr int B_CH = BN * BK / 8 / kGemmThreads;
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  bf16_t* As = reinterpret_cast<bf16_t*>(smem);          // [2][BM][kLDK]
-  bf16_t* Bs = As + 2 * BM * kLDK;                        // [2][BN][kLDK]
+  constexpr int THREADS = NW * 64;
+  constexpr int TM = BM / 32;
+  constexpr int BN = 32 * NW;                     // NW waves x 32 columns
+  constexpr int LDA = kBK + 8;                    // padded LDS row (bf16 elements)
+  constexpr int A_CH = BM * kBK / 8 / THREADS;
+  constexpr int LDC = 33;                         // padded row of a wave's 32 columns
+  static_assert(NW % 4 == 0 && A_CH >= 1, "tile shape");
+  // LDS: the double-buffered activation tile, reused after the K loop by the ARGMAX
+  // epilogue to stage the fp32 tile of four waves at a time ([wave][row][32 columns]).
+  constexpr size_t kMainLds = size_t(2) * BM * LDA * sizeof(bf16_t);
+  constexpr size_t kEpiLds = (EPI == kEpiArgmax) ? size_t(4) * BM * LDC * sizeof(float) : 0;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kMainLds > kEpiLds ? kMainLds : kEpiLds];
+  typedef bf16_t ATile[BM][LDA];
+  ATile* As = reinterpret_cast<ATile*>(smem);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wid = tid >> 6;
-  const int wm = wid / WN, wn = wid % WN;
 
   const int mt = (p.M + BM - 1) / BM;
   const int nt = (p.N + BN - 1) / BN;
@@ -116,98 +81,88 @@ gemm_bf16_kernel(GemmArgs p) {
   const int n_tile = tile / mt, m_tile = tile % mt;
   const int m0 = m_tile * BM, n0 = n_tile * BN;
 
-  const int nk_all = p.K / BK;
+  const int nk_all = p.K / kBK;
   const int z = blockIdx.z;
   const int kt_begin = (nk_all * z) / gridDim.z;
   const int kt_end = (nk_all * (z + 1)) / gridDim.z;
   const int nk = kt_end - kt_begin;
 
   const bf16_t* A = static_cast<const bf16_t*>(p.A);
-  const bf16_t* B = static_cast<const bf16_t*>(p.B);
+  // This wave's 32-row block of a 128-row weight group (rows past N are zero padding
+  // of the packed layout; a group past the last one is clamped to it, and the columns
+  // it computes are never stored).
+  const int n_groups = (p.N + 127) >> 7;
+  const int grp = min(n_tile * (NW / 4) + (wid >> 2), n_groups - 1);
+  const bf16_t* Bw = static_cast<const bf16_t*>(p.B) +
+                     (int64_t(grp) * (p.K >> 4) * 4 + (wid & 3)) * 512 + lane * 8;
 
-  u32x4 ra[STAGES][A_CH], rb[STAGES][B_CH];
-
-  // Rows past M (or N) are clamped to the last valid row rather than predicated: they
-  // only feed accumulator rows/columns that are never stored, and unpredicated loads
-  // keep the compiler's outstanding-load counting exact, so the prefetched stages stay
-  // in flight across iterations.
-  // A wave instruction covers 64 / CPR rows x CPR*16 contiguous bytes of each row.
-  auto gload = [&](int kt, u32x4* da, u32x4* db) {
-    const int64_t k = int64_t(kt_begin + kt) * BK;
-#pragma unroll
-    for (int i = 0; i < A_CH; ++i) {
-      const int c = tid + i * kGemmThreads;
-      const int row = min(m0 + c / CPR, p.M - 1), col = (c % CPR) * 8;
-      da[i] = ld16(A + int64_t(row) * p.lda + k + col);
-    }
-#pragma unroll
-    for (int i = 0; i < B_CH; ++i) {
-      const int c = tid + i * kGemmThreads;
-      const int row = min(n0 + c / CPR, p.N - 1), col = (c % CPR) * 8;
-      db[i] = ld16(B + int64_t(row) * p.ldb + k + col);
-    }
-  };
-  auto sstore = [&](const u32x4* da, const u32x4* db, int buf) {
-#pragma unroll
-    for (int i = 0; i < A_CH; ++i) {
-      const int c = tid + i * kGemmThreads;
-      const int row = c / CPR, col = (c % CPR) * 8;
-      *reinterpret_cast<u32x4*>(As + (buf * BM + row) * kLDK + col) = da[i];
-    }
-#pragma unroll
-    for (int i = 0; i < B_CH; ++i) {
-      const int c = tid + i * kGemmThreads;
-      const int row = c / CPR, col = (c % CPR) * 8;
-      *reinterpret_cast<u32x4*>(Bs + (buf * BN + row) * kLDK + col) = db[i];
-    }
-  };
-
-  f32x16_t acc[TM][TN];
+  f32x16_t acc[TM];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
 
   if (nk > 0) {
-    const int arow = wm * (BM / WM) + (lane & 31);
-    const int brow = wn * (BN / WN) + (lane & 31);
-    const int kof = 8 * (lane >> 5);
-    auto compute = [&](int buf) {
-      const bf16_t* as = As + buf * BM * kLDK;
-      const bf16_t* bs = Bs + buf * BN * kLDK;
+    u32x4 ra[STAGES][A_CH];
+    u32x4 rb[STAGES][4];
+    // Activation chunk c of a K-step: row c/8, 16-byte column c%8.  Rows past M are
+    // clamped (their products are never stored); loads stay unpredicated so the
+    // compiler's outstanding-load counting is exact.
+    auto load_a = [&](int kt, u32x4* dst) {
+      const int64_t k = int64_t(kt_begin + min(kt, nk - 1)) * kBK;
 #pragma unroll
-      for (int ks = 0; ks < BK / 16; ++ks) {
-        bf16x8_t af[TM], bfr[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          af[i] = *reinterpret_cast<const bf16x8_t*>(as + (arow + i * 32) * kLDK + ks * 16 + kof);
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          bfr[j] = *reinterpret_cast<const bf16x8_t*>(bs + (brow + j * 32) * kLDK + ks * 16 + kof);
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+      for (int i = 0; i < A_CH; ++i) {
+        const int c = tid + i * THREADS;
+        const int row = min(m0 + (c >> 3), p.M - 1);
+        dst[i] = ld16(A + int64_t(row) * p.lda + k + (c & 7) * 8);
       }
     };
-    // One K-tile step with ring slot u (a compile-time constant after unrolling):
-    // refill slot u with tile t+STAGES (tile t is already in LDS), compute tile t,
-    // move tile t+1 from its slot into the other LDS buffer, barrier.  Tile indices
-    // past the end are clamped to the last tile (an L2 hit, never used), so every
-    // load and store is unconditional.
+    auto load_b = [&](int kt, u32x4* dst) {
+      const int64_t kb = int64_t(kt_begin + min(kt, nk - 1)) * (kBK / 16);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) dst[q] = ld_nt16(Bw + (kb + q) * 4 * 512);
+    };
+    auto store_a = [&](const u32x4* src, int buf) {
+#pragma unroll
+      for (int i = 0; i < A_CH; ++i) {
+        const int c = tid + i * THREADS;
+        *reinterpret_cast<u32x4*>(&As[buf][c >> 3][(c & 7) * 8]) = src[i];
+      }
+    };
+    const int arow = lane & 31;
+    const int kof = 8 * (lane >> 5);
+    auto compute = [&](int buf, const u32x4* bq) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const bf16x8_t bf = __builtin_bit_cast(bf16x8_t, bq[q]);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const bf16x8_t af =
+              *reinterpret_cast<const bf16x8_t*>(&As[buf][arow + 32 * i][q * 16 + kof]);
+          acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bf, acc[i], 0, 0, 0);
+        }
+      }
+    };
+    // Prologue: A(0) into LDS; then A(1..STAGES) and B(0..STAGES-1), interleaved in the
+    // order they are consumed.
+    load_a(0, ra[0]);
+    store_a(ra[0], 0);
+#pragma unroll
+    for (int st = 0; st < STAGES; ++st) {
+      load_a(st + 1, ra[(st + 1) % STAGES]);
+      load_b(st, rb[st]);
+    }
+    __syncthreads();
+    // Step t (ring slot u = t % STAGES): compute with A(t) in LDS and B(t) in rb[u];
+    // move A(t+1) into the other LDS buffer; refill the freed slots with A(t+1+STAGES)
+    // and B(t+STAGES); barrier.
     auto step = [&](int t, int u) {
-      gload(min(t + STAGES, nk - 1), ra[u], rb[u]);
-      compute(t & 1);
-      sstore(ra[(u + 1) % STAGES], rb[(u + 1) % STAGES], (t + 1) & 1);
+      compute(t & 1, rb[u]);
+      store_a(ra[(u + 1) % STAGES], (t + 1) & 1);
+      load_a(t + 1 + STAGES, ra[(u + 1) % STAGES]);
+      load_b(t + STAGES, rb[u]);
       __syncthreads();
     };
-#pragma unroll
-    for (int st = 0; st < STAGES; ++st) gload(min(st, nk - 1), ra[st], rb[st]);
-    sstore(ra[0], rb[0], 0);
-    __syncthreads();
     int kt = 0;
     for (; kt + STAGES <= nk; kt += STAGES) {
 #pragma unroll
@@ -218,47 +173,83 @@ gemm_bf16_kernel(GemmArgs p) {
       if (kt + u < nk) step(kt + u, u);
   }
 
+  const int col = n0 + 32 * wid + (lane & 31);
   if constexpr (EPI == kEpiPartial) {
     float* C = p.C + int64_t(z) * p.M * p.N;
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int col = n0 + wn * (BN / WN) + j * 32 + (lane & 31);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = m0 + wm * (BM / WM) + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-          if (row < p.M && col < p.N) C[int64_t(row) * p.N + col] = acc[i][j][r];
-        }
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (row < p.M && col < p.N) C[int64_t(row) * p.N + col] = acc[i][r];
       }
   } else {
-    constexpr int LDC = BN + 4;
+    // Stage the fp32 tile in LDS, four waves (128 columns) at a time ([wave][row][column
+    // of the wave]); THREADS/BM threads per row scan each 128-column slab (lowest column
+    // on ties), and one atomic per row folds the tile's (max, index) into the row's
+    // packed key.  The K loop ended with a barrier, so the activation buffers are free.
     float* Cs = reinterpret_cast<float*>(smem);
-    // The last loop iteration ended with a barrier, so LDS is free.
+    constexpr int TPR = THREADS / BM;        // threads per row
+    constexpr int CPT = 128 / TPR;           // columns of a slab per thread
+    const int rl = tid / TPR, part = tid % TPR;
+    float best = -INFINITY;
+    int bcol = 0x7FFFFFFF;
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int slab = 0; slab < NW / 4; ++slab) {
+      if (slab > 0) __syncthreads();
+      if ((wid >> 2) == slab) {
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int col = wn * (BN / WN) + j * 32 + (lane & 31);
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = wm * (BM / WM) + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-          Cs[row * LDC + col] = acc[i][j][r];
+          for (int r = 0; r < 16; ++r) {
+            const int rr = 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            Cs[((wid & 3) * BM + rr) * LDC + (lane & 31)] = acc[i][r];
+          }
+      }
+      __syncthreads();
+      const int c0 = n0 + 128 * slab;
+      if (m0 + rl < p.M) {
+        for (int cc = part * CPT; cc < part * CPT + CPT; ++cc) {
+          if (c0 + cc >= p.N) break;
+          const float v = Cs[((cc >> 5) * BM + rl) * LDC + (cc & 31)];
+          if (v > best) {
+            best = v;
+            bcol = c0 + cc;
+          }
         }
       }
-    __syncthreads();
-    argmax_epilogue<BM, BN, LDC>(Cs, m0, n0, p.M, p.N, p.keys, p.C);
+      if (p.C != nullptr) {
+        // Logits (tests): coalesced rows of the staged slab.
+        for (int e = tid; e < BM * 128; e += THREADS) {
+          const int rr = e >> 7, cc = e & 127;
+          if (m0 + rr < p.M && c0 + cc < p.N)
+            p.C[int64_t(m0 + rr) * p.N + c0 + cc] = Cs[((cc >> 5) * BM + rr) * LDC + (cc & 31)];
+        }
+      }
+    }
+#pragma unroll
+    for (int o = 1; o < TPR; o <<= 1) {
+      const float ov = __shfl_xor(best, o, kWave);
+      const int oc = __shfl_xor(bcol, o, kWave);
+      if (ov > best || (ov == best && oc < bcol)) {
+        best = ov;
+        bcol = oc;
+      }
+    }
+    if (part == 0 && m0 + rl < p.M && bcol != 0x7FFFFFFF)
+      atomicMax(p.keys + m0 + rl, argmax_key(best, bcol));
   }
 }
 
-// fp32 operands: 64x64 tiles, BK = 16, each thread owns a 4x4 block of C.
+// fp32 operands: 64x64 tiles, BK = 16, each thread owns a 4x4 block of C; the
+// weights are read through the packed index.
 template <int EPI>
 __global__ void __launch_bounds__(kGemmThreads)
 gemm_f32_kernel(GemmArgs p) {
   constexpr int BM = 64, BN = 64, BKF = 16;
   __shared__ float As[BKF][BM + 4];
   __shared__ float Bs[BKF][BN + 4];
-  __shared__ float Cs[BM * (BN + 4)];
+  __shared__ float Cs[BM][BN + 4];
   const int tid = threadIdx.x;
   const int tx = tid % 16, ty = tid / 16;
   const int mt = (p.M + BM - 1) / BM;
@@ -277,7 +268,7 @@ gemm_f32_kernel(GemmArgs p) {
     for (int i = tid; i < BM * BKF; i += kGemmThreads) {
       const int r = i / BKF, kk = i % BKF;
       As[kk][r] = (m0 + r < p.M) ? A[int64_t(m0 + r) * p.lda + k0 + kk] : 0.f;
-      Bs[kk][r] = (n0 + r < p.N) ? B[int64_t(n0 + r) * p.ldb + k0 + kk] : 0.f;
+      Bs[kk][r] = (n0 + r < p.N) ? B[packed_index(n0 + r, k0 + kk, p.K)] : 0.f;
     }
     __syncthreads();
 #pragma unroll
@@ -307,9 +298,36 @@ gemm_f32_kernel(GemmArgs p) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) Cs[(ty * 4 + i) * (BN + 4) + tx * 4 + j] = c[i][j];
+      for (int j = 0; j < 4; ++j) Cs[ty * 4 + i][tx * 4 + j] = c[i][j];
     __syncthreads();
-    argmax_epilogue<BM, BN, BN + 4>(Cs, m0, n0, p.M, p.N, p.keys, p.C);
+    // Four threads per row, 16 columns each, lowest column on ties.
+    const int r = tid >> 2, part = tid & 3;
+    float best = -INFINITY;
+    int bcol = 0x7FFFFFFF;
+    if (m0 + r < p.M) {
+      for (int cc = part * 16; cc < part * 16 + 16; ++cc) {
+        const int gcol = n0 + cc;
+        if (gcol < p.N) {
+          const float v = Cs[r][cc];
+          if (p.C != nullptr) p.C[int64_t(m0 + r) * p.N + gcol] = v;
+          if (v > best) {
+            best = v;
+            bcol = gcol;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int o = 1; o < 4; o <<= 1) {
+      const float ov = __shfl_xor(best, o, kWave);
+      const int oc = __shfl_xor(bcol, o, kWave);
+      if (ov > best || (ov == best && oc < bcol)) {
+        best = ov;
+        bcol = oc;
+      }
+    }
+    if (part == 0 && m0 + r < p.M && bcol != 0x7FFFFFFF)
+      atomicMax(p.keys + m0 + r, argmax_key(best, bcol));
   }
 }
 
@@ -327,42 +345,53 @@ __global__ void argmax_finalize_kernel(const unsigned long long* keys, int64_t M
   if (max_logit != nullptr) max_logit[i] = f32_from_order_key(uint32_t(k >> 32));
 }
 
+// Row-major [N][K] -> packed layout, one 16-byte (bf16) or 32-byte (fp32) lane chunk
+// of 8 elements per thread; rows N..ceil(N/128)*128-1 are written as zeros.
+template <typename T>
+__global__ void pack_weight_kernel(const T* __restrict__ src, T* __restrict__ dst, int N, int K) {
+  const int64_t chunks = int64_t((N + 127) / 128) * (K / 16) * 4 * 64;
+  for (int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; e < chunks;
+       e += int64_t(gridDim.x) * blockDim.x) {
+    const int lane = int(e & 63);
+    const int64_t blk = e >> 6;                 // ((group * (K/16)) + kb) * 4 + sub
+    const int sub = int(blk & 3);
+    const int64_t kb = (blk >> 2) % (K / 16), grp = (blk >> 2) / (K / 16);
+    const int64_t n = grp * 128 + sub * 32 + (lane & 31);
+    const int64_t k = kb * 16 + 8 * (lane >> 5);
+    T* d = dst + e * 8;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) d[j] = (n < N) ? src[n * K + k + j] : T(0);
+  }
+}
+
 // ---------------------------------------------------------------------------- host side
 
-template <typename K>
-static hipError_t set_lds(K kern, size_t bytes) {
-  if (bytes <= 65536) return hipSuccess;
-  // Once per kernel instantiation (the attribute is per function, not per device).
-  static std::atomic<bool> done{false};
-  if (done.load(std::memory_order_acquire)) return hipSuccess;
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, int(bytes));
-  if (e == hipSuccess) done.store(true, std::memory_order_release);
-  return e;
-}
-
-template <int BM, int EPI>
-static hipError_t launch_bf16(const GemmArgs& a, int splits, hipStream_t s) {
-  constexpr int BN = 128, BK = kBK, STAGES = 3;
-  auto kern = gemm_bf16_kernel<BM, BN, BK, STAGES, EPI>;
-  const size_t main_lds = size_t(2) * (BM + BN) * (BK + 8) * sizeof(bf16_t);
-  const size_t epi_lds = (EPI == kEpiPartial) ? 0 : size_t(BM) * (BN + 4) * sizeof(float);
-  const size_t lds = main_lds > epi_lds ? main_lds : epi_lds;
-  hipError_t e = set_lds(kern, lds);
-  if (e != hipSuccess) return e;
-  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL(kern, dim3(tiles, 1, splits), dim3(kGemmThreads), lds, s, a);
-  return hipGetLastError();
-}
+// Waves per workgroup of the bf16 kernel (32 weight rows each).  Wider workgroups read
+// the activation tile once for more weight rows: the LM head streams 1 GB of weights
+// against a 1 MB activation block that every column tile re-reads from L2.
+constexpr int kPartialWaves = 4;
+constexpr int kArgmaxWaves = 8;
+static int gemm_waves(int epi) { return epi == kEpiPartial ? kPartialWaves : kArgmaxWaves; }
 
 static hipError_t launch_gemm_any(bool bf16, int epi, const GemmArgs& a, int splits,
                                   hipStream_t s) {
   if (bf16) {
-    if (a.M <= 64)
-      return epi == kEpiPartial ? launch_bf16<64, kEpiPartial>(a, splits, s)
-                                : launch_bf16<64, kEpiArgmax>(a, splits, s);
-    return epi == kEpiPartial ? launch_bf16<128, kEpiPartial>(a, splits, s)
-                              : launch_bf16<128, kEpiArgmax>(a, splits, s);
+    const int BM = a.M <= 64 ? 64 : 128;
+    const int NW = gemm_waves(epi);
+    const int tiles = ((a.M + BM - 1) / BM) * ((a.N + 32 * NW - 1) / (32 * NW));
+    const dim3 grid(tiles, 1, splits), block(NW * 64);
+    if (a.M <= 64) {
+      if (epi == kEpiPartial)
+        hipLaunchKernelGGL((gemm_bf16_kernel<64, kPartialWaves, 4, kEpiPartial>), grid, block, 0, s, a);
+      else
+        hipLaunchKernelGGL((gemm_bf16_kernel<64, kArgmaxWaves, 2, kEpiArgmax>), grid, block, 0, s, a);
+    } else {
+      if (epi == kEpiPartial)
+        hipLaunchKernelGGL((gemm_bf16_kernel<128, kPartialWaves, 4, kEpiPartial>), grid, block, 0, s, a);
+      else
+        hipLaunchKernelGGL((gemm_bf16_kernel<128, kArgmaxWaves, 2, kEpiArgmax>), grid, block, 0, s, a);
+    }
+    return hipGetLastError();
   }
   const int tiles = ((a.M + 63) / 64) * ((a.N + 63) / 64);
   if (epi == kEpiPartial)
@@ -378,7 +407,7 @@ int gemm_k_align(bool bf16) { return bf16 ? kBK : 16; }
 
 int gemm_pick_splits(bool bf16, int M, int N, int K) {
   const int BM = bf16 ? (M <= 64 ? 64 : 128) : 64;
-  const int BN = bf16 ? 128 : 64;
+  const int BN = bf16 ? 32 * gemm_waves(kEpiPartial) : 64;
   const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
   const int nk = K / gemm_k_align(bf16);
   // One wave of workgroups over the CUs; every split keeps at least 8 K-tiles and the
@@ -391,10 +420,26 @@ int gemm_pick_splits(bool bf16, int M, int N, int K) {
   return s < 1 ? 1 : s;
 }
 
-hipError_t launch_gemm_partial(bool bf16, const void* A, int64_t lda, const void* B, int64_t ldb,
-                               int M, int N, int K, int splits, float* C, hipStream_t s) {
+size_t packed_weight_elems(int N, int K) { return size_t((N + 127) / 128) * 128 * size_t(K); }
+
+hipError_t launch_pack_weight(bool bf16, const void* src, void* dst, int N, int K, hipStream_t s) {
+  const int64_t chunks = int64_t((N + 127) / 128) * (K / 16) * 4 * 64;
+  int64_t blocks = (chunks + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  if (blocks < 1) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL(pack_weight_kernel<bf16_t>, dim3(unsigned(blocks)), dim3(256), 0, s,
+                       static_cast<const bf16_t*>(src), static_cast<bf16_t*>(dst), N, K);
+  else
+    hipLaunchKernelGGL(pack_weight_kernel<float>, dim3(unsigned(blocks)), dim3(256), 0, s,
+                       static_cast<const float*>(src), static_cast<float*>(dst), N, K);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_partial(bool bf16, const void* A, int64_t lda, const void* B, int M, int N,
+                               int K, int splits, float* C, hipStream_t s) {
   GemmArgs a{};
-  a.A = A; a.lda = lda; a.B = B; a.ldb = ldb;
+  a.A = A; a.lda = lda; a.B = B;
   a.M = M; a.N = N; a.K = K; a.C = C; a.keys = nullptr;
   return launch_gemm_any(bf16, kEpiPartial, a, splits, s);
 }
@@ -414,7 +459,7 @@ hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t 
     GemmArgs a{};
     const size_t el = bf16 ? 2 : 4;
     a.A = static_cast<const char*>(hidden) + r0 * d * el;
-    a.lda = d; a.B = W; a.ldb = d;
+    a.lda = d; a.B = W;
     a.M = rows; a.N = V; a.K = d;
     a.C = logits != nullptr ? logits + r0 * V : nullptr;
     a.keys = keys + r0;

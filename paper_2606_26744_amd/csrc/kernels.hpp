@@ -29,10 +29,9 @@ constexpr int kEpiPartial = 0;  // fp32 C / split-K partials
 constexpr int kEpiArgmax = 1;   // LM head: fused row argmax (+ optional fp32 logits in C)
 
 struct GemmArgs {
-  const void* A;
+  const void* A;   // [M][lda] row-major activations
   int64_t lda;
-  const void* B;
-  int64_t ldb;
+  const void* B;   // [N][K] weights in the packed layout (hdf_pack_weight)
   int M, N, K;
   float* C;
   unsigned long long* keys;
@@ -40,9 +39,11 @@ struct GemmArgs {
 
 int gemm_k_align(bool bf16);                       // K must be a multiple of this
 int gemm_pick_splits(bool bf16, int M, int N, int K);
-// C[z][M][N] (fp32) = A[M][K] . B[N][K]^T over the z-th of `splits` K ranges.
-hipError_t launch_gemm_partial(bool bf16, const void* A, int64_t lda, const void* B, int64_t ldb,
-                               int M, int N, int K, int splits, float* C, hipStream_t s);
+size_t packed_weight_elems(int N, int K);          // rows rounded up to 128
+hipError_t launch_pack_weight(bool bf16, const void* src, void* dst, int N, int K, hipStream_t s);
+// C[z][M][N] (fp32) = A[M][K] . W[N][K]^T over the z-th of `splits` K ranges; W packed.
+hipError_t launch_gemm_partial(bool bf16, const void* A, int64_t lda, const void* B, int M, int N,
+                               int K, int splits, float* C, hipStream_t s);
 // keys: M 64-bit scratch words.  logits may be NULL.
 hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t M, int d, int V,
                           unsigned long long* keys, int32_t* argmax, float* max_logit,

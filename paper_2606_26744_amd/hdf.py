@@ -22,6 +22,7 @@ STATUS = {0: "HDF_OK", 1: "HDF_E_INVALID", 2: "HDF_E_UNSUPPORTED", 3: "HDF_E_WOR
 
 # Every symbol include/hdf.h declares.
 EXPORTS = ("hdf_last_error", "hdf_version", "hdf_hc_reduce", "hdf_rope_table",
+           "hdf_packed_weight_bytes", "hdf_pack_weight",
            "hdf_kv_cache_bytes", "hdf_draft_block_workspace", "hdf_draft_block",
            "hdf_lm_head_workspace", "hdf_lm_head_argmax", "hdf_accept")
 
@@ -73,6 +74,10 @@ def lib() -> ctypes.CDLL:
     L.hdf_hc_reduce.argtypes = [_P, _P, _P, _I64, _I, _I, _I, ctypes.POINTER(ReduceParams), _P, _P, _P]
     L.hdf_rope_table.restype = _I
     L.hdf_rope_table.argtypes = [_P, _I, _I, ctypes.c_double]
+    L.hdf_packed_weight_bytes.restype = _SZ
+    L.hdf_packed_weight_bytes.argtypes = [_I, _I, _I]
+    L.hdf_pack_weight.restype = _I
+    L.hdf_pack_weight.argtypes = [_P, _P, _I, _I, _I, _P]
     L.hdf_kv_cache_bytes.restype = _SZ
     L.hdf_kv_cache_bytes.argtypes = [ctypes.POINTER(Drafter), _I64]
     L.hdf_draft_block_workspace.restype = _SZ
@@ -163,19 +168,51 @@ def accept(draft: torch.Tensor, target: torch.Tensor, *, K: Optional[int] = None
     return acc, anc, offs, toks
 
 
+# ----------------------------------------------------------------------------- weights
+
+class PackedWeight:
+    """A weight W[N][K] in the library's packed layout (hdf_pack_weight)."""
+
+    def __init__(self, data: torch.Tensor, N: int, K: int):
+        self.data, self.N, self.K = data, N, K
+
+    @property
+    def dtype(self):
+        return self.data.dtype
+
+    def data_ptr(self):
+        return self.data.data_ptr()
+
+
+def pack_weight(w: torch.Tensor, stream=None) -> PackedWeight:
+    """Packs a row-major [N][K] device weight with hdf_pack_weight."""
+    N, K = w.shape
+    _dev(w)
+    nbytes = int(lib().hdf_packed_weight_bytes(N, K, _dt(w)))
+    if nbytes == 0:
+        raise ValueError(f"cannot pack a {N} x {K} weight (K must be a multiple of 16)")
+    out = torch.empty(nbytes // w.element_size(), dtype=w.dtype, device=w.device)
+    _check(lib().hdf_pack_weight(_ptr(w), _ptr(out), N, K, _dt(w), _stream(stream)))
+    return PackedWeight(out, N, K)
+
+
 # ----------------------------------------------------------------------------- LM head
 
 def lm_head_workspace(M: int, vocab: int) -> int:
     return int(lib().hdf_lm_head_workspace(M, vocab))
 
 
-def lm_head_argmax(hidden: torch.Tensor, w_lm: torch.Tensor, *, want_logits: bool = False,
+def lm_head_argmax(hidden: torch.Tensor, w_lm: PackedWeight, *, want_logits: bool = False,
                    want_max: bool = True, ws: Optional[torch.Tensor] = None, out=None,
                    stream=None):
-    """hdf_lm_head_argmax: hidden [M, d], w_lm [V, d] -> (argmax int32 [M], max fp32 [M],
-    logits fp32 [M, V] or None)."""
+    """hdf_lm_head_argmax: hidden [M, d], packed w_lm [V, d] -> (argmax int32 [M], max fp32
+    [M], logits fp32 [M, V] or None)."""
+    if not isinstance(w_lm, PackedWeight):
+        raise TypeError("w_lm must be packed with pack_weight()")
     M, d = hidden.shape
-    V = w_lm.shape[0]
+    V = w_lm.N
+    if w_lm.K != d or w_lm.dtype != hidden.dtype:
+        raise ValueError("hidden and w_lm disagree in width or dtype")
     dev = hidden.device
     if out is None:
         am = torch.empty(M, dtype=torch.int32, device=dev)
@@ -186,7 +223,7 @@ def lm_head_argmax(hidden: torch.Tensor, w_lm: torch.Tensor, *, want_logits: boo
     need = lm_head_workspace(M, V)
     if ws is None or ws.numel() < need:
         ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-    _dev(hidden, w_lm, am, mx, lg, ws)
+    _dev(hidden, w_lm.data, am, mx, lg, ws)
     _check(lib().hdf_lm_head_argmax(_ptr(hidden), _ptr(w_lm), M, d, V, _dt(hidden), _ptr(am),
                                     _ptr(mx), _ptr(lg), _ptr(ws), ws.numel(), _stream(stream)))
     return am, mx, lg
@@ -202,7 +239,8 @@ def rope_table(n_pos: int, head_dim: int, theta: float) -> torch.Tensor:
 
 
 class DrafterHandle:
-    """Keeps the device weights and the ctypes hdf_drafter struct alive together."""
+    """Keeps the device weights (projections packed once, here) and the ctypes
+    hdf_drafter struct alive together."""
 
     def __init__(self, weights: dict, *, n_layers: int, d: int, n_heads: int, head_dim: int,
                  d_ff: int, vocab: int, eps: float = 1e-6, rope_theta: float = 10000.0,
@@ -210,6 +248,9 @@ class DrafterHandle:
         self.w = weights
         self.L = n_layers
         dt = weights["tok_emb"].dtype
+        self.packed = {k: [pack_weight(x).data for x in weights[k]]
+                       for k in ("w_qkv", "w_o", "w_gate_up", "w_down")}
+        self.w_lm = pack_weight(weights["w_lm"]) if weights.get("w_lm") is not None else None
         self.torch_dtype = dt
         keep = []
 
@@ -225,9 +266,9 @@ class DrafterHandle:
             n_layers, d, n_heads, head_dim, d_ff, vocab, _dt(weights["tok_emb"]), eps,
             weights["tok_emb"].data_ptr(),
             None if weights.get("ctx_norm") is None else weights["ctx_norm"].data_ptr(),
-            arr(weights.get("attn_norm", [None] * n_layers)), arr(weights["w_qkv"]),
-            arr(weights["w_o"]), arr(weights.get("mlp_norm", [None] * n_layers)),
-            arr(weights["w_gate_up"]), arr(weights["w_down"]),
+            arr(weights.get("attn_norm", [None] * n_layers)), arr(self.packed["w_qkv"]),
+            arr(self.packed["w_o"]), arr(weights.get("mlp_norm", [None] * n_layers)),
+            arr(self.packed["w_gate_up"]), arr(self.packed["w_down"]),
             None if weights.get("final_norm") is None else weights["final_norm"].data_ptr(),
             None if self.rope is None else self.rope.data_ptr(),
             rope_max_pos if self.rope is not None else 0)

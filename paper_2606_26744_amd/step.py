@@ -57,7 +57,7 @@ def drafter_step(handle: hdf.DrafterHandle, bufs: StepBuffers, *, H_new: torch.T
                        kv_offsets=kv_offsets, kv_k=kv_k, kv_vt=kv_vt, tokens=tokens,
                        hidden=bufs.hidden, ws=bufs.ws, stream=stream)
     mark(2)
-    am, mx, lg = hdf.lm_head_argmax(bufs.hidden, handle.w["w_lm"], want_logits=logits,
+    am, mx, lg = hdf.lm_head_argmax(bufs.hidden, handle.w_lm, want_logits=logits,
                                     ws=bufs.lm_ws, out=(bufs.argmax, bufs.max_logit),
                                     stream=stream)
     mark(3)

@@ -84,3 +84,15 @@ def test_rope_table_host_values():
     buf = (ctypes.c_float * 64)()
     assert _status(L.hdf_rope_table(buf, 4, 7, 1e4)) == "HDF_E_INVALID"
     assert _status(L.hdf_rope_table(buf, 4, 8, 0.0)) == "HDF_E_INVALID"
+
+
+def test_pack_weight_validation():
+    L = hdf.lib()
+    fake = ctypes.c_void_p(4096)
+    assert L.hdf_packed_weight_bytes(70, 48, 1) == 128 * 48 * 2
+    assert L.hdf_packed_weight_bytes(70, 40, 1) == 0          # K % 16 != 0
+    assert L.hdf_packed_weight_bytes(0, 48, 0) == 0
+    assert _status(L.hdf_pack_weight(fake, None, 70, 48, 1, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_pack_weight(fake, fake, 70, 48, 1, None)) == "HDF_E_INVALID"   # in place
+    assert _status(L.hdf_pack_weight(fake, ctypes.c_void_p(8192), 70, 40, 1, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_pack_weight(fake, ctypes.c_void_p(8192), 70, 48, 5, None)) == "HDF_E_INVALID"

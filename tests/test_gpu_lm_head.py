@@ -24,7 +24,7 @@ def _inputs(M, d, V, dtype, seed):
 def _check(hid, w, rows=None, want_logits=True, dtype="bf16"):
     M, V = hid.shape[0], w.shape[0]
     print(f"[lm_head] M={M} d={hid.shape[1]} V={V} dtype={dtype}", flush=True)
-    am, mx, lg = hdf.lm_head_argmax(hid, w, want_logits=want_logits)
+    am, mx, lg = hdf.lm_head_argmax(hid, hdf.pack_weight(w), want_logits=want_logits)
     torch.cuda.synchronize()
     sel = np.arange(M) if rows is None else np.asarray(rows)
     r_am, r_lg, r_margin = ref_lm(synth.to_numpy_bits(hid)[sel], synth.to_numpy_bits(w))
@@ -78,20 +78,39 @@ def test_ties_take_lowest_index():
     w[2999] = w[17]
     w[1200] = w[17]
     hid[0] = (w[17].float() * 40).to(torch.bfloat16)   # row 0's maximum is the tied row
-    am, _, lg = hdf.lm_head_argmax(hid, w, want_logits=True)
+    am, _, lg = hdf.lm_head_argmax(hid, hdf.pack_weight(w), want_logits=True)
     assert am[0].item() == 17
     assert lg[0, 17].item() == lg[0, 1200].item() == lg[0, 2999].item()
+
+
+def test_pack_weight_layout():
+    """The packed layout puts (n, k) at (((n/128)(K/16) + k/16)*4 + (n%128)/32)*512
+    + ((n%32) + 32((k%16)/8))*8 + k%8 and pads rows to a multiple of 128 with zeros."""
+    for dt in (torch.bfloat16, torch.float32):
+        N, K = 170, 48
+        w = torch.randn(N, K, generator=torch.Generator().manual_seed(5)).to(dt).cuda()
+        p = hdf.pack_weight(w).data.cpu()
+        R = 256
+        assert p.numel() == R * K
+        n = torch.arange(R).view(-1, 1)
+        k = torch.arange(K).view(1, -1)
+        idx = (((n // 128) * (K // 16) + k // 16) * 4 + (n % 128) // 32) * 512 + \
+            ((n % 32) + 32 * ((k % 16) // 8)) * 8 + k % 8
+        got = p[idx.reshape(-1)].view(R, K)
+        assert torch.equal(got[:N], w.cpu())
+        assert torch.all(got[N:] == 0)
 
 
 def test_empty():
     hid = torch.empty((0, 128), dtype=torch.bfloat16, device="cuda")
     w = torch.zeros((10, 128), dtype=torch.bfloat16, device="cuda")
-    am, _, _ = hdf.lm_head_argmax(hid, w)
+    am, _, _ = hdf.lm_head_argmax(hid, hdf.pack_weight(w))
     assert am.numel() == 0
 
 
 def test_determinism():
     hid, w = _inputs(128, 1024, 32000, "bf16", 64)
-    a1, m1, l1 = hdf.lm_head_argmax(hid, w, want_logits=True)
-    a2, m2, l2 = hdf.lm_head_argmax(hid, w, want_logits=True)
+    wp = hdf.pack_weight(w)
+    a1, m1, l1 = hdf.lm_head_argmax(hid, wp, want_logits=True)
+    a2, m2, l2 = hdf.lm_head_argmax(hid, wp, want_logits=True)
     assert torch.equal(a1, a2) and torch.equal(m1, m2) and torch.equal(l1, l2)
