@@ -220,6 +220,11 @@ size_t hdf_lm_head_workspace(int64_t M, int vocab);
  * argmax    [M] int32 (out)
  * max_logit [M] fp32 (out, may be NULL)
  * logits    [M][vocab] fp32 (out, may be NULL; for tests)
+ * ws, ws_bytes  at least hdf_lm_head_workspace(M, vocab) bytes, 8-byte aligned,
+ *           holding zeros before its first use (allocate it zero-filled); every call
+ *           hands it back zeroed (it holds the per-row argmax keys the kernels fold
+ *           into), so it can be reused as is.  Calls sharing a workspace must not run
+ *           concurrently.
  * Limits: d % 64 == 0; 1 <= vocab < 2^31; M >= 0. */
 hdf_status hdf_lm_head_argmax(const void* hidden, const void* W_lm, int64_t M, int d, int vocab,
                               hdf_dtype dtype, int32_t* argmax, float* max_logit, float* logits,

@@ -289,36 +289,41 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
     if (e != hipSuccess) return hip_fail(e, #x);    \
   } while (0)
 
-  // Context rows projected in this call: (position, cache row) per row, then in
-  // chunks: c = RMSNorm(y) * ctx_norm and, per layer, K/V into the cache.
-  if (n_new > 0) {
-    HDF_TRY(hdf::launch_plan_rows(ctx_len, new_offsets, kv_offsets, n_seq, n_new, plan_pos,
-                                  plan_row, s));
-    for (int64_t r0 = 0; r0 < n_new; r0 += kCtxChunk) {
-      const int rows = int(n_new - r0 < kCtxChunk ? n_new - r0 : kCtxChunk);
-      HDF_TRY(hdf::launch_row_norm(bf, static_cast<const char*>(y_new) + r0 * d * el, w->ctx_norm,
-                                   w->eps, rows, d, cbuf, s));
-      for (int l = 0; l < L; ++l) {
-        // Rows d..3d-1 (W_k; W_v) of the packed W_qkv: d/128 whole row groups in.
-        const char* wkv = static_cast<const char*>(w->w_qkv[l]) + size_t(d) * d * el;
-        const int S = hdf::gemm_pick_splits(bf, rows, 2 * d, d);
-        HDF_TRY(hdf::launch_gemm_partial(bf, cbuf, d, wkv, rows, 2 * d, d, S, parts, s));
-        hdf::QkvEpiArgs ea{};
-        ea.parts = parts; ea.S = S; ea.M = rows; ea.first_part = 1;
-        ea.d = d; ea.nh = nh; ea.hd = hd; ea.B = B;
-        ea.ctx_len = ctx_len; ea.plan_pos = plan_pos + r0; ea.plan_row = plan_row + r0;
-        ea.rope_cs = w->rope_cs;
-        ea.q = nullptr;
-        ea.k = static_cast<char*>(kv_k) + l * layer_kv;
-        ea.vt = static_cast<char*>(kv_vt) + l * layer_kv;
-        ea.cap = kv_cap;
-        HDF_TRY(hdf::launch_qkv_epilogue(bf, ea, s));
-      }
+  // First kernel: context rows r0.. (position, cache row; RMSNorm(y) * ctx_norm) and,
+  // with the first chunk, the block rows (h = emb[tokens]; u = RMSNorm(h) * attn_norm[0]).
+  auto prep = [&](int64_t r0, int rows, bool block) {
+    hdf::PrepArgs pa{};
+    pa.y = y_new; pa.r0 = r0; pa.n_ctx = rows; pa.ctx_gamma = w->ctx_norm; pa.c = cbuf;
+    pa.ctx_len = ctx_len; pa.new_offsets = new_offsets; pa.kv_offsets = kv_offsets;
+    pa.n_seq = n_seq; pa.plan_pos = plan_pos; pa.plan_row = plan_row;
+    pa.n_blk = block ? M : 0; pa.tokens = tokens; pa.emb = w->tok_emb;
+    pa.attn_gamma = w->attn_norm[0]; pa.h = h; pa.u = u;
+    pa.d = d; pa.eps = w->eps;
+    return hdf::launch_prep(bf, pa, s);
+  };
+  // Context rows projected in this call, in chunks: K/V of every layer into the cache.
+  if (n_new == 0) HDF_TRY(prep(0, 0, true));
+  for (int64_t r0 = 0; r0 < n_new; r0 += kCtxChunk) {
+    const int rows = int(n_new - r0 < kCtxChunk ? n_new - r0 : kCtxChunk);
+    HDF_TRY(prep(r0, rows, r0 == 0));
+    for (int l = 0; l < L; ++l) {
+      // Rows d..3d-1 (W_k; W_v) of the packed W_qkv: d/128 whole row groups in.
+      const char* wkv = static_cast<const char*>(w->w_qkv[l]) + size_t(d) * d * el;
+      const int S = hdf::gemm_pick_splits(bf, rows, 2 * d, d);
+      HDF_TRY(hdf::launch_gemm_partial(bf, cbuf, d, wkv, rows, 2 * d, d, S, parts, s));
+      hdf::QkvEpiArgs ea{};
+      ea.parts = parts; ea.S = S; ea.M = rows; ea.first_part = 1;
+      ea.d = d; ea.nh = nh; ea.hd = hd; ea.B = B;
+      ea.ctx_len = ctx_len; ea.plan_pos = plan_pos + r0; ea.plan_row = plan_row + r0;
+      ea.rope_cs = w->rope_cs;
+      ea.q = nullptr;
+      ea.k = static_cast<char*>(kv_k) + l * layer_kv;
+      ea.vt = static_cast<char*>(kv_vt) + l * layer_kv;
+      ea.cap = kv_cap;
+      HDF_TRY(hdf::launch_qkv_epilogue(bf, ea, s));
     }
   }
 
-  // Block: h = emb[tokens]; u = RMSNorm(h) * attn_norm[0].
-  HDF_TRY(hdf::launch_embed_norm(bf, tokens, w->tok_emb, w->attn_norm[0], w->eps, M, d, h, u, s));
   const int n_chunks = (max_ctx + P.chunk_len - 1) / P.chunk_len;
   for (int l = 0; l < L; ++l) {
     // Q, K_b, V_b with RoPE at T_s + k.

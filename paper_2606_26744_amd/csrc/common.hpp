@@ -68,6 +68,17 @@ __device__ __forceinline__ void st_nt16(void* p, u32x4 v) {
   __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
 }
 
+// SiLU(g) * u, the gated MLP activation.
+__device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.f + __expf(-g)) * u; }
+
+// Rotate-half RoPE of the pair (x1, x2) = (x[i], x[i + hd/2]) by the angle with
+// cosine c and sine s.
+__device__ __forceinline__ void rope_rotate(float& x1, float& x2, float c, float s) {
+  const float u1 = x1, u2 = x2;
+  x1 = u1 * c - u2 * s;
+  x2 = u2 * c + u1 * s;
+}
+
 // Order-preserving map of a finite fp32 to uint32 (larger float -> larger key).
 __device__ __forceinline__ uint32_t f32_order_key(float f) {
   uint32_t u = __float_as_uint(f);

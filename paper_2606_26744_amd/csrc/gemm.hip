@@ -331,18 +331,14 @@ gemm_f32_kernel(GemmArgs p) {
   }
 }
 
-__global__ void argmax_init_kernel(unsigned long long* keys, int64_t M) {
-  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i < M) keys[i] = 0ull;
-}
-
-__global__ void argmax_finalize_kernel(const unsigned long long* keys, int64_t M, int32_t* argmax,
+__global__ void argmax_finalize_kernel(unsigned long long* keys, int64_t M, int32_t* argmax,
                                        float* max_logit) {
   const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i >= M) return;
   const unsigned long long k = keys[i];
   argmax[i] = int32_t(0xFFFFFFFFu - uint32_t(k & 0xFFFFFFFFull));
   if (max_logit != nullptr) max_logit[i] = f32_from_order_key(uint32_t(k >> 32));
+  keys[i] = 0ull;   // the workspace is handed back zeroed
 }
 
 // Row-major [N][K] -> packed layout, one 16-byte (bf16) or 32-byte (fp32) lane chunk
@@ -447,11 +443,10 @@ hipError_t launch_gemm_partial(bool bf16, const void* A, int64_t lda, const void
 hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t M, int d, int V,
                           unsigned long long* keys, int32_t* argmax, float* max_logit,
                           float* logits, hipStream_t s) {
+  // keys are zero on entry (the workspace contract): the finalize pass clears them.
   const int threads = 256;
   const unsigned blocks = unsigned((M + threads - 1) / threads);
-  hipLaunchKernelGGL(argmax_init_kernel, dim3(blocks), dim3(threads), 0, s, keys, M);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  hipError_t e;
   // Rows are processed in chunks that keep the int32 tile arithmetic in range.
   const int64_t chunk = 1 << 20;
   for (int64_t r0 = 0; r0 < M; r0 += chunk) {

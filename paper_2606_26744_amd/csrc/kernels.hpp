@@ -65,15 +65,30 @@ struct QkvEpiArgs {
   int64_t cap;
 };
 
-hipError_t launch_plan_rows(const int32_t* ctx_len, const int32_t* new_offsets,
-                            const int32_t* kv_offsets, int n_seq, int64_t n_new, int32_t* plan_pos,
-                            int32_t* plan_row, hipStream_t s);
-// out = RMSNorm(in) * gamma, row-wise, in/out in the working dtype.
-hipError_t launch_row_norm(bool bf16, const void* in, const float* gamma, float eps, int64_t rows,
-                           int d, void* out, hipStream_t s);
-// h = float(emb[tokens]); u = RMSNorm(h) * gamma
-hipError_t launch_embed_norm(bool bf16, const int32_t* tokens, const void* emb, const float* gamma,
-                             float eps, int64_t rows, int d, float* h, void* u, hipStream_t s);
+struct PrepArgs {
+  // context rows r0 .. r0+n_ctx-1 of y_new: plan_pos/plan_row[r] and c[r - r0]
+  const void* y;
+  int64_t r0;
+  int n_ctx;
+  const float* ctx_gamma;
+  void* c;
+  const int32_t* ctx_len;
+  const int32_t* new_offsets;
+  const int32_t* kv_offsets;
+  int n_seq;
+  int32_t* plan_pos;
+  int32_t* plan_row;
+  // block rows (n_blk of them, or none): h = float(emb[tokens]), u = RMSNorm(h) * attn_gamma
+  int n_blk;
+  const int32_t* tokens;
+  const void* emb;
+  const float* attn_gamma;
+  float* h;
+  void* u;
+  int d;
+  float eps;
+};
+hipError_t launch_prep(bool bf16, const PrepArgs& a, hipStream_t s);
 // h += sum_z parts[z]; u = RMSNorm(h) * gamma
 hipError_t launch_residual_norm(bool bf16, const float* parts, int S, const float* gamma, float eps,
                                 int64_t rows, int d, float* h, void* u, hipStream_t s);

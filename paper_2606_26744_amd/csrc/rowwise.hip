@@ -1,7 +1,8 @@
-// Row-wise kernels of the block drafter: RMSNorms, the token-embedding gather,
-// split-K reduction fused with the residual update and the next RMSNorm, the
-// projection epilogues (RoPE + scatter into the attention layouts, SiLU gate)
-// and the per-row plan of the context rows projected in this step.
+// Row-wise kernels of the block drafter: the call's first kernel (per-row plan of
+// the context rows projected in this call, their RMSNorm, the token-embedding
+// gather and the block's first RMSNorm), split-K reduction fused with the residual
+// update and the next RMSNorm, and the projection epilogues (RoPE + scatter into
+// the attention layouts, SiLU gate).
 //
 // All are HBM/L2-bound elementwise passes over rows of width d: one 256-thread
 // workgroup per row (norm kernels) with 16-byte or 8-byte accesses, fp32
@@ -56,68 +57,64 @@ __device__ __forceinline__ float block_sum(float v, float* sh) {
 // Rows are at most 8192 wide: 8 groups of 4 per thread at 256 threads.
 constexpr int kMaxGroups = 8;
 
+// First kernel of a drafter call, one 256-thread workgroup per row:
+//   context rows: (position, cache row) of the row, c = RMSNorm(y) * ctx_norm;
+//   block rows:   h = float(emb[token]), u = RMSNorm(h) * attn_norm[0].
 template <typename T>
 __global__ void __launch_bounds__(kRowThreads)
-row_norm_kernel(const T* __restrict__ in, const float* __restrict__ gamma, float eps, int d,
-                T* __restrict__ out) {
+prep_kernel(PrepArgs a) {
   __shared__ float sh[kRowThreads / 64];
-  const int64_t r = blockIdx.x;
-  const T* x = in + r * d;
+  const int b = blockIdx.x;
+  const T* x;
+  float* hrow = nullptr;
+  const float* gamma;
+  T* out;
+  if (b < a.n_ctx) {
+    const int64_t r = a.r0 + b;
+    if (threadIdx.x == 0) {
+      int lo = 0, hi = a.n_seq - 1;   // last s with new_offsets[s] <= r
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (a.new_offsets[mid] <= r) lo = mid; else hi = mid - 1;
+      }
+      const int ns = a.new_offsets[lo + 1] - a.new_offsets[lo];
+      const int pos = a.ctx_len[lo] - ns + int(r - a.new_offsets[lo]);
+      a.plan_pos[r] = pos;
+      a.plan_row[r] = a.kv_offsets[lo] + pos;
+    }
+    x = static_cast<const T*>(a.y) + r * a.d;
+    gamma = a.ctx_gamma;
+    out = static_cast<T*>(a.c) + int64_t(b) * a.d;
+  } else {
+    const int64_t r = b - a.n_ctx;
+    x = static_cast<const T*>(a.emb) + int64_t(a.tokens[r]) * a.d;
+    hrow = a.h + r * a.d;
+    gamma = a.attn_gamma;
+    out = static_cast<T*>(a.u) + r * a.d;
+  }
   float v[kMaxGroups][4];
   float ss = 0.f;
 #pragma unroll
   for (int g = 0; g < kMaxGroups; ++g) {
     const int c = (g * kRowThreads + threadIdx.x) * 4;
-    if (c < d) {
+    if (c < a.d) {
       load4<T>(x + c, v[g]);
+      if (hrow != nullptr)
+        *reinterpret_cast<float4*>(hrow + c) = make_float4(v[g][0], v[g][1], v[g][2], v[g][3]);
 #pragma unroll
       for (int j = 0; j < 4; ++j) ss = fmaf(v[g][j], v[g][j], ss);
     }
   }
   ss = block_sum(ss, sh);
-  const float rs = rsqrtf(ss / float(d) + eps);
+  const float rs = rsqrtf(ss / float(a.d) + a.eps);
 #pragma unroll
   for (int g = 0; g < kMaxGroups; ++g) {
     const int c = (g * kRowThreads + threadIdx.x) * 4;
-    if (c < d) {
+    if (c < a.d) {
       float o[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) o[j] = v[g][j] * rs * (gamma ? gamma[c + j] : 1.f);
-      store4<T>(out + r * d + c, o);
-    }
-  }
-}
-
-template <typename T>
-__global__ void __launch_bounds__(kRowThreads)
-embed_norm_kernel(const int32_t* __restrict__ tokens, const T* __restrict__ emb,
-                  const float* __restrict__ gamma, float eps, int d, float* __restrict__ h,
-                  T* __restrict__ u) {
-  __shared__ float sh[kRowThreads / 64];
-  const int64_t r = blockIdx.x;
-  const T* x = emb + int64_t(tokens[r]) * d;
-  float v[kMaxGroups][4];
-  float ss = 0.f;
-#pragma unroll
-  for (int g = 0; g < kMaxGroups; ++g) {
-    const int c = (g * kRowThreads + threadIdx.x) * 4;
-    if (c < d) {
-      load4<T>(x + c, v[g]);
-      *reinterpret_cast<float4*>(h + r * d + c) = make_float4(v[g][0], v[g][1], v[g][2], v[g][3]);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) ss = fmaf(v[g][j], v[g][j], ss);
-    }
-  }
-  ss = block_sum(ss, sh);
-  const float rs = rsqrtf(ss / float(d) + eps);
-#pragma unroll
-  for (int g = 0; g < kMaxGroups; ++g) {
-    const int c = (g * kRowThreads + threadIdx.x) * 4;
-    if (c < d) {
-      float o[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) o[j] = v[g][j] * rs * (gamma ? gamma[c + j] : 1.f);
-      store4<T>(u + r * d + c, o);
+      store4<T>(out + c, o);
     }
   }
 }
@@ -165,26 +162,6 @@ residual_norm_kernel(const float* __restrict__ parts, int S, int64_t M,
       store4<T>(u + r * d + c, o);
     }
   }
-}
-
-// Rows of y_new -> (position, cache row): sequence s owns rows new_offsets[s] ..
-// new_offsets[s+1]-1, which are its last n_s context positions.
-__global__ void plan_rows_kernel(const int32_t* __restrict__ ctx_len,
-                                 const int32_t* __restrict__ new_offsets,
-                                 const int32_t* __restrict__ kv_offsets, int n_seq, int64_t n_new,
-                                 int32_t* __restrict__ plan_pos, int32_t* __restrict__ plan_row) {
-  const int64_t r = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (r >= n_new) return;
-  int lo = 0, hi = n_seq - 1;  // last s with new_offsets[s] <= r
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (new_offsets[mid] <= r) lo = mid; else hi = mid - 1;
-  }
-  const int s = lo;
-  const int ns = new_offsets[s + 1] - new_offsets[s];
-  const int pos = ctx_len[s] - ns + int(r - new_offsets[s]);
-  plan_pos[r] = pos;
-  plan_row[r] = kv_offsets[s] + pos;
 }
 
 __device__ __forceinline__ void row_dest(const QkvEpiArgs& a, int r, int& pos, int64_t& drow,
@@ -257,11 +234,7 @@ qkv_epilogue_kernel(QkvEpiArgs a) {
       const float cv[4] = {cs01.x, cs01.z, cs23.x, cs23.z};
       const float sv[4] = {cs01.y, cs01.w, cs23.y, cs23.w};
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float u1 = y1[j], u2 = y2[j];
-        y1[j] = u1 * cv[j] - u2 * sv[j];
-        y2[j] = u2 * cv[j] + u1 * sv[j];
-      }
+      for (int j = 0; j < 4; ++j) rope_rotate(y1[j], y2[j], cv[j], sv[j]);
     }
     T* dst;
     if (part == 0)
@@ -316,45 +289,20 @@ silu_kernel(const float* __restrict__ parts, int S, int64_t M, int F, T* __restr
     }
     float o[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) o[j] = g[j] / (1.f + __expf(-g[j])) * u[j];
+    for (int j = 0; j < 4; ++j) o[j] = silu_mul(g[j], u[j]);
     store4<T>(act + idx, o);
   }
 }
 
 // ---------------------------------------------------------------------------- host side
 
-hipError_t launch_plan_rows(const int32_t* ctx_len, const int32_t* new_offsets,
-                            const int32_t* kv_offsets, int n_seq, int64_t n_new, int32_t* plan_pos,
-                            int32_t* plan_row, hipStream_t s) {
-  if (n_new <= 0) return hipSuccess;
-  hipLaunchKernelGGL(plan_rows_kernel, dim3(unsigned((n_new + 255) / 256)), dim3(256), 0, s,
-                     ctx_len, new_offsets, kv_offsets, n_seq, n_new, plan_pos, plan_row);
-  return hipGetLastError();
-}
-
-hipError_t launch_row_norm(bool bf16, const void* in, const float* gamma, float eps, int64_t rows,
-                           int d, void* out, hipStream_t s) {
-  if (rows <= 0) return hipSuccess;
+hipError_t launch_prep(bool bf16, const PrepArgs& a, hipStream_t s) {
+  const int64_t wgs = int64_t(a.n_ctx) + a.n_blk;
+  if (wgs <= 0) return hipSuccess;
   if (bf16)
-    hipLaunchKernelGGL(row_norm_kernel<bf16_t>, dim3(unsigned(rows)), dim3(kRowThreads), 0, s,
-                       static_cast<const bf16_t*>(in), gamma, eps, d, static_cast<bf16_t*>(out));
+    hipLaunchKernelGGL(prep_kernel<bf16_t>, dim3(unsigned(wgs)), dim3(kRowThreads), 0, s, a);
   else
-    hipLaunchKernelGGL(row_norm_kernel<float>, dim3(unsigned(rows)), dim3(kRowThreads), 0, s,
-                       static_cast<const float*>(in), gamma, eps, d, static_cast<float*>(out));
-  return hipGetLastError();
-}
-
-hipError_t launch_embed_norm(bool bf16, const int32_t* tokens, const void* emb, const float* gamma,
-                             float eps, int64_t rows, int d, float* h, void* u, hipStream_t s) {
-  if (rows <= 0) return hipSuccess;
-  if (bf16)
-    hipLaunchKernelGGL(embed_norm_kernel<bf16_t>, dim3(unsigned(rows)), dim3(kRowThreads), 0, s,
-                       tokens, static_cast<const bf16_t*>(emb), gamma, eps, d, h,
-                       static_cast<bf16_t*>(u));
-  else
-    hipLaunchKernelGGL(embed_norm_kernel<float>, dim3(unsigned(rows)), dim3(kRowThreads), 0, s,
-                       tokens, static_cast<const float*>(emb), gamma, eps, d, h,
-                       static_cast<float*>(u));
+    hipLaunchKernelGGL(prep_kernel<float>, dim3(unsigned(wgs)), dim3(kRowThreads), 0, s, a);
   return hipGetLastError();
 }
 

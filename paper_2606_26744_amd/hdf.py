@@ -222,7 +222,7 @@ def lm_head_argmax(hidden: torch.Tensor, w_lm: PackedWeight, *, want_logits: boo
     lg = torch.empty((M, V), dtype=torch.float32, device=dev) if want_logits else None
     need = lm_head_workspace(M, V)
     if ws is None or ws.numel() < need:
-        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        ws = torch.zeros(max(need, 1), dtype=torch.uint8, device=dev)   # zero before first use
     _dev(hidden, w_lm.data, am, mx, lg, ws)
     _check(lib().hdf_lm_head_argmax(_ptr(hidden), _ptr(w_lm), M, d, V, _dt(hidden), _ptr(am),
                                     _ptr(mx), _ptr(lg), _ptr(ws), ws.numel(), _stream(stream)))

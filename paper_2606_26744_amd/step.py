@@ -28,8 +28,8 @@ class StepBuffers:
         self.hidden = torch.empty((n_seq * B, d), dtype=dt, device=device)
         self.ws = torch.empty(max(handle.workspace_bytes(n_seq, B, n_new, max_ctx), 1),
                               dtype=torch.uint8, device=device)
-        self.lm_ws = torch.empty(max(hdf.lm_head_workspace(n_seq * B, handle.V), 1),
-                                 dtype=torch.uint8, device=device)
+        self.lm_ws = torch.zeros(max(hdf.lm_head_workspace(n_seq * B, handle.V), 1),
+                                 dtype=torch.uint8, device=device)   # zero before first use
         self.argmax = torch.empty(n_seq * B, dtype=torch.int32, device=device)
         self.max_logit = torch.empty(n_seq * B, dtype=torch.float32, device=device)
 
