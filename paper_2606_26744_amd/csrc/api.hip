@@ -107,7 +107,7 @@ DraftPlan plan_workspace(const hdf_drafter& w, int n_seq, int B, int64_t n_new, 
   size_t parts = 0;
   auto upd = [&](int64_t rows, int N, int K) {
     if (rows <= 0) return;
-    const size_t sp = size_t(hdf::gemm_pick_splits(bf, int(rows), N, K));
+    const size_t sp = size_t(hdf::gemm_plan(bf, int(rows), N, K).splits);
     const size_t b = sp * size_t(rows) * size_t(N) * 4;
     if (b > parts) parts = b;
   };
@@ -309,8 +309,9 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
     for (int l = 0; l < L; ++l) {
       // Rows d..3d-1 (W_k; W_v) of the packed W_qkv: d/128 whole row groups in.
       const char* wkv = static_cast<const char*>(w->w_qkv[l]) + size_t(d) * d * el;
-      const int S = hdf::gemm_pick_splits(bf, rows, 2 * d, d);
-      HDF_TRY(hdf::launch_gemm_partial(bf, cbuf, d, wkv, rows, 2 * d, d, S, parts, s));
+      const hdf::GemmPlan Sp = hdf::gemm_plan(bf, rows, 2 * d, d);
+    const int S = Sp.splits;
+      HDF_TRY(hdf::launch_gemm_partial(bf, cbuf, d, wkv, rows, 2 * d, d, Sp, parts, s));
       hdf::QkvEpiArgs ea{};
       ea.parts = parts; ea.S = S; ea.M = rows; ea.first_part = 1;
       ea.d = d; ea.nh = nh; ea.hd = hd; ea.B = B;
@@ -327,8 +328,9 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
   const int n_chunks = (max_ctx + P.chunk_len - 1) / P.chunk_len;
   for (int l = 0; l < L; ++l) {
     // Q, K_b, V_b with RoPE at T_s + k.
-    const int Sq = hdf::gemm_pick_splits(bf, M, 3 * d, d);
-    HDF_TRY(hdf::launch_gemm_partial(bf, u, d, w->w_qkv[l], M, 3 * d, d, Sq, parts, s));
+    const hdf::GemmPlan Sqp = hdf::gemm_plan(bf, M, 3 * d, d);
+    const int Sq = Sqp.splits;
+    HDF_TRY(hdf::launch_gemm_partial(bf, u, d, w->w_qkv[l], M, 3 * d, d, Sqp, parts, s));
     hdf::QkvEpiArgs ea{};
     ea.parts = parts; ea.S = Sq; ea.M = M; ea.first_part = 0;
     ea.d = d; ea.nh = nh; ea.hd = hd; ea.B = B;
@@ -349,16 +351,19 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
     HDF_TRY(hdf::launch_attention(bf, aa, attn, s));
 
     // h += O Wo^T; u = RMSNorm(h) * mlp_norm.
-    const int So = hdf::gemm_pick_splits(bf, M, d, d);
-    HDF_TRY(hdf::launch_gemm_partial(bf, attn, d, w->w_o[l], M, d, d, So, parts, s));
+    const hdf::GemmPlan Sop = hdf::gemm_plan(bf, M, d, d);
+    const int So = Sop.splits;
+    HDF_TRY(hdf::launch_gemm_partial(bf, attn, d, w->w_o[l], M, d, d, Sop, parts, s));
     HDF_TRY(hdf::launch_residual_norm(bf, parts, So, w->mlp_norm[l], w->eps, M, d, h, u, s));
 
     // act = SiLU(u Wg^T) * (u Wu^T); h += act Wd^T; next norm.
-    const int Sg = hdf::gemm_pick_splits(bf, M, 2 * F, d);
-    HDF_TRY(hdf::launch_gemm_partial(bf, u, d, w->w_gate_up[l], M, 2 * F, d, Sg, parts, s));
+    const hdf::GemmPlan Sgp = hdf::gemm_plan(bf, M, 2 * F, d);
+    const int Sg = Sgp.splits;
+    HDF_TRY(hdf::launch_gemm_partial(bf, u, d, w->w_gate_up[l], M, 2 * F, d, Sgp, parts, s));
     HDF_TRY(hdf::launch_silu_epilogue(bf, parts, Sg, M, F, act, s));
-    const int Sd = hdf::gemm_pick_splits(bf, M, d, F);
-    HDF_TRY(hdf::launch_gemm_partial(bf, act, F, w->w_down[l], M, d, F, Sd, parts, s));
+    const hdf::GemmPlan Sdp = hdf::gemm_plan(bf, M, d, F);
+    const int Sd = Sdp.splits;
+    HDF_TRY(hdf::launch_gemm_partial(bf, act, F, w->w_down[l], M, d, F, Sdp, parts, s));
     const bool last = (l + 1 == L);
     HDF_TRY(hdf::launch_residual_norm(bf, parts, Sd, last ? w->final_norm : w->attn_norm[l + 1],
                                       w->eps, M, d, h, last ? hidden : u, s));

@@ -60,9 +60,10 @@ gemm_bf16_kernel(GemmArgs p) {
   constexpr int TM = BM / 32;
   constexpr int BN = 32 * NW;                     // NW waves x 32 columns
   constexpr int LDA = kBK + 8;                    // padded LDS row (bf16 elements)
-  constexpr int A_CH = BM * kBK / 8 / THREADS;
+  constexpr int A_CHUNKS = BM * kBK / 8;           // 16-byte chunks of an activation step
+  constexpr int A_CH = (A_CHUNKS + THREADS - 1) / THREADS;
   constexpr int LDC = 33;                         // padded row of a wave's 32 columns
-  static_assert(NW % 4 == 0 && A_CH >= 1, "tile shape");
+  static_assert(EPI != kEpiArgmax || NW % 4 == 0, "argmax tiles are whole 4-wave slabs");
   // LDS: the double-buffered activation tile, reused after the K loop by the ARGMAX
   // epilogue to stage the fp32 tile of four waves at a time ([wave][row][32 columns]).
   constexpr size_t kMainLds = size_t(2) * BM * LDA * sizeof(bf16_t);
@@ -88,13 +89,14 @@ gemm_bf16_kernel(GemmArgs p) {
   const int nk = kt_end - kt_begin;
 
   const bf16_t* A = static_cast<const bf16_t*>(p.A);
-  // This wave's 32-row block of a 128-row weight group (rows past N are zero padding
-  // of the packed layout; a group past the last one is clamped to it, and the columns
-  // it computes are never stored).
+  // This wave's 32-row weight block: block b = n_tile*NW + wid is sub-block b%4 of
+  // 128-row group b/4 (rows past N are zero padding of the packed layout; a group past
+  // the last one is clamped to it, and the columns it computes are never stored).
   const int n_groups = (p.N + 127) >> 7;
-  const int grp = min(n_tile * (NW / 4) + (wid >> 2), n_groups - 1);
+  const int blk = n_tile * NW + wid;
+  const int grp = min(blk >> 2, n_groups - 1);
   const bf16_t* Bw = static_cast<const bf16_t*>(p.B) +
-                     (int64_t(grp) * (p.K >> 4) * 4 + (wid & 3)) * 512 + lane * 8;
+                     (int64_t(grp) * (p.K >> 4) * 4 + (blk & 3)) * 512 + lane * 8;
 
   f32x16_t acc[TM];
 #pragma unroll
@@ -112,7 +114,7 @@ gemm_bf16_kernel(GemmArgs p) {
       const int64_t k = int64_t(kt_begin + min(kt, nk - 1)) * kBK;
 #pragma unroll
       for (int i = 0; i < A_CH; ++i) {
-        const int c = tid + i * THREADS;
+        const int c = min(tid + i * THREADS, A_CHUNKS - 1);   // spare threads repeat the last
         const int row = min(m0 + (c >> 3), p.M - 1);
         dst[i] = ld16(A + int64_t(row) * p.lda + k + (c & 7) * 8);
       }
@@ -125,7 +127,7 @@ gemm_bf16_kernel(GemmArgs p) {
     auto store_a = [&](const u32x4* src, int buf) {
 #pragma unroll
       for (int i = 0; i < A_CH; ++i) {
-        const int c = tid + i * THREADS;
+        const int c = min(tid + i * THREADS, A_CHUNKS - 1);
         *reinterpret_cast<u32x4*>(&As[buf][c >> 3][(c & 7) * 8]) = src[i];
       }
     };
@@ -362,28 +364,32 @@ __global__ void pack_weight_kernel(const T* __restrict__ src, T* __restrict__ ds
 
 // ---------------------------------------------------------------------------- host side
 
-// Waves per workgroup of the bf16 kernel (32 weight rows each).  Wider workgroups read
-// the activation tile once for more weight rows: the LM head streams 1 GB of weights
-// against a 1 MB activation block that every column tile re-reads from L2.
-constexpr int kPartialWaves = 4;
 constexpr int kArgmaxWaves = 8;
-static int gemm_waves(int epi) { return epi == kEpiPartial ? kPartialWaves : kArgmaxWaves; }
 
-static hipError_t launch_gemm_any(bool bf16, int epi, const GemmArgs& a, int splits,
+template <int NW>
+static void launch_bf16_partial(const GemmArgs& a, int splits, hipStream_t s) {
+  const int BM = a.M <= 64 ? 64 : 128;
+  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + 32 * NW - 1) / (32 * NW));
+  const dim3 grid(tiles, 1, splits), block(NW * 64);
+  if (BM == 64)
+    hipLaunchKernelGGL((gemm_bf16_kernel<64, NW, 4, kEpiPartial>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, 4, kEpiPartial>), grid, block, 0, s, a);
+}
+
+static hipError_t launch_gemm_any(bool bf16, int epi, const GemmArgs& a, GemmPlan plan,
                                   hipStream_t s) {
   if (bf16) {
-    const int BM = a.M <= 64 ? 64 : 128;
-    const int NW = gemm_waves(epi);
-    const int tiles = ((a.M + BM - 1) / BM) * ((a.N + 32 * NW - 1) / (32 * NW));
-    const dim3 grid(tiles, 1, splits), block(NW * 64);
-    if (a.M <= 64) {
-      if (epi == kEpiPartial)
-        hipLaunchKernelGGL((gemm_bf16_kernel<64, kPartialWaves, 4, kEpiPartial>), grid, block, 0, s, a);
-      else
-        hipLaunchKernelGGL((gemm_bf16_kernel<64, kArgmaxWaves, 2, kEpiArgmax>), grid, block, 0, s, a);
+    if (epi == kEpiPartial) {
+      if (plan.nw == 8) launch_bf16_partial<8>(a, plan.splits, s);
+      else if (plan.nw == 6) launch_bf16_partial<6>(a, plan.splits, s);
+      else launch_bf16_partial<4>(a, plan.splits, s);
     } else {
-      if (epi == kEpiPartial)
-        hipLaunchKernelGGL((gemm_bf16_kernel<128, kPartialWaves, 4, kEpiPartial>), grid, block, 0, s, a);
+      const int BM = a.M <= 64 ? 64 : 128;
+      const int tiles = ((a.M + BM - 1) / BM) * ((a.N + 32 * kArgmaxWaves - 1) / (32 * kArgmaxWaves));
+      const dim3 grid(tiles, 1, 1), block(kArgmaxWaves * 64);
+      if (BM == 64)
+        hipLaunchKernelGGL((gemm_bf16_kernel<64, kArgmaxWaves, 2, kEpiArgmax>), grid, block, 0, s, a);
       else
         hipLaunchKernelGGL((gemm_bf16_kernel<128, kArgmaxWaves, 2, kEpiArgmax>), grid, block, 0, s, a);
     }
@@ -391,29 +397,54 @@ static hipError_t launch_gemm_any(bool bf16, int epi, const GemmArgs& a, int spl
   }
   const int tiles = ((a.M + 63) / 64) * ((a.N + 63) / 64);
   if (epi == kEpiPartial)
-    hipLaunchKernelGGL(gemm_f32_kernel<kEpiPartial>, dim3(tiles, 1, splits), dim3(kGemmThreads), 0,
-                       s, a);
+    hipLaunchKernelGGL(gemm_f32_kernel<kEpiPartial>, dim3(tiles, 1, plan.splits),
+                       dim3(kGemmThreads), 0, s, a);
   else
-    hipLaunchKernelGGL(gemm_f32_kernel<kEpiArgmax>, dim3(tiles, 1, splits), dim3(kGemmThreads), 0,
-                       s, a);
+    hipLaunchKernelGGL(gemm_f32_kernel<kEpiArgmax>, dim3(tiles, 1, 1), dim3(kGemmThreads), 0, s,
+                       a);
   return hipGetLastError();
 }
 
 int gemm_k_align(bool bf16) { return bf16 ? kBK : 16; }
 
-int gemm_pick_splits(bool bf16, int M, int N, int K) {
-  const int BM = bf16 ? (M <= 64 ? 64 : 128) : 64;
-  const int BN = bf16 ? 32 * gemm_waves(kEpiPartial) : 64;
-  const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+GemmPlan gemm_plan(bool bf16, int M, int N, int K) {
+  const int ncu = device_cu_count();
   const int nk = K / gemm_k_align(bf16);
-  // One wave of workgroups over the CUs; every split keeps at least 8 K-tiles and the
-  // fp32 partials (S * M * N * 4 bytes, read back once) stay small next to the weights.
-  const int target = device_cu_count();
-  int s = (target + tiles - 1) / tiles;
-  const int max_s = nk / 8 > 1 ? nk / 8 : 1;
-  if (s > max_s) s = max_s;
-  if (s > 8) s = 8;
-  return s < 1 ? 1 : s;
+  if (!bf16) {
+    const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
+    int s = (ncu + tiles - 1) / tiles;
+    const int max_s = nk / 8 > 1 ? nk / 8 : 1;
+    s = s > max_s ? max_s : (s > 8 ? 8 : s);
+    return GemmPlan{4, s < 1 ? 1 : s};
+  }
+  // One workgroup per CU works best for these weight streams: a CU holding two
+  // workgroups while others hold one doubles the kernel's critical path.  Pick the
+  // tile width (4, 6 or 8 waves of 32 columns) and K split whose workgroup count fills
+  // the CUs best without exceeding them; ties go to fewer splits (less partial
+  // traffic) and then to more waves (more bytes in flight per CU).  Every split keeps
+  // at least 8 K-steps.
+  const int BM = M <= 64 ? 64 : 128;
+  const int mt = (M + BM - 1) / BM;
+  GemmPlan best{4, 1};
+  double best_fill = -1.0;
+  for (int nw : {4, 6, 8}) {
+    const int tiles = mt * ((N + 32 * nw - 1) / (32 * nw));
+    for (int s = 1; s <= 16; ++s) {
+      if (s > 1 && nk / s < 8) break;
+      const int wgs = tiles * s;
+      const int rounds = (wgs + ncu - 1) / ncu;
+      const double fill = double(wgs) / double(rounds * ncu);   // busy fraction of CU-rounds
+      // Prefer a single round; more rounds only when they are nearly full.
+      const double score = fill / rounds + (rounds == 1 ? 1.0 : 0.0);
+      const bool tie = score > best_fill - 1e-9 && score < best_fill + 1e-9;
+      if (score > best_fill + 1e-9 ||
+          (tie && (s < best.splits || (s == best.splits && nw > best.nw)))) {
+        best_fill = score;
+        best = GemmPlan{nw, s};
+      }
+    }
+  }
+  return best;
 }
 
 size_t packed_weight_elems(int N, int K) { return size_t((N + 127) / 128) * 128 * size_t(K); }
@@ -433,11 +464,11 @@ hipError_t launch_pack_weight(bool bf16, const void* src, void* dst, int N, int 
 }
 
 hipError_t launch_gemm_partial(bool bf16, const void* A, int64_t lda, const void* B, int M, int N,
-                               int K, int splits, float* C, hipStream_t s) {
+                               int K, GemmPlan plan, float* C, hipStream_t s) {
   GemmArgs a{};
   a.A = A; a.lda = lda; a.B = B;
   a.M = M; a.N = N; a.K = K; a.C = C; a.keys = nullptr;
-  return launch_gemm_any(bf16, kEpiPartial, a, splits, s);
+  return launch_gemm_any(bf16, kEpiPartial, a, plan, s);
 }
 
 hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t M, int d, int V,
@@ -458,7 +489,7 @@ hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t 
     a.M = rows; a.N = V; a.K = d;
     a.C = logits != nullptr ? logits + r0 * V : nullptr;
     a.keys = keys + r0;
-    e = launch_gemm_any(bf16, kEpiArgmax, a, 1, s);
+    e = launch_gemm_any(bf16, kEpiArgmax, a, GemmPlan{kArgmaxWaves, 1}, s);
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(argmax_finalize_kernel, dim3(blocks), dim3(threads), 0, s, keys, M, argmax,

@@ -38,12 +38,17 @@ struct GemmArgs {
 };
 
 int gemm_k_align(bool bf16);                       // K must be a multiple of this
-int gemm_pick_splits(bool bf16, int M, int N, int K);
+// Launch shape of a partial-sum GEMM: waves per workgroup (32 columns each; bf16:
+// 4, 6 or 8) and the number of K splits.
+struct GemmPlan {
+  int nw, splits;
+};
+GemmPlan gemm_plan(bool bf16, int M, int N, int K);
 size_t packed_weight_elems(int N, int K);          // rows rounded up to 128
 hipError_t launch_pack_weight(bool bf16, const void* src, void* dst, int N, int K, hipStream_t s);
 // C[z][M][N] (fp32) = A[M][K] . W[N][K]^T over the z-th of `splits` K ranges; W packed.
 hipError_t launch_gemm_partial(bool bf16, const void* A, int64_t lda, const void* B, int M, int N,
-                               int K, int splits, float* C, hipStream_t s);
+                               int K, GemmPlan plan, float* C, hipStream_t s);
 // keys: M 64-bit scratch words.  logits may be NULL.
 hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t M, int d, int V,
                           unsigned long long* keys, int32_t* argmax, float* max_logit,

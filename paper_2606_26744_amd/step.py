@@ -42,12 +42,13 @@ def drafter_step(handle: hdf.DrafterHandle, bufs: StepBuffers, *, H_new: torch.T
                  stream=None, logits: bool = False, marks: Optional[list] = None):
     """Runs reduce -> draft block -> LM head argmax -> accept.  Returns a dict of device
     tensors (Y, hidden, argmax, max_logit, and accept outputs when targets are given).
-    marks: optional list of five timing events recorded on the stream around the stages."""
+    marks: optional list of five timing events (entries may be None) recorded on the stream
+    around the stages."""
     kw = dict(reduce_kw or {})
     kw.setdefault("eps", handle.eps)
 
     def mark(i):
-        if marks is not None:
+        if marks is not None and marks[i] is not None:
             marks[i].record(stream if stream is not None else torch.cuda.current_stream())
 
     mark(0)
