@@ -165,16 +165,20 @@ typedef struct {
  * The caller copies it to the device once and passes it as hdf_drafter.rope_cs. */
 hdf_status hdf_rope_table(float* out_host, int n_pos, int head_dim, double theta);
 
-/* KV cache, caller-owned, `dtype` elements:
- *   k  [n_layers][n_heads][kv_cap][head_dim]           keys after RoPE
- *   vt [n_layers][n_heads][kv_cap/64][head_dim][64]    values in tiles of 64 positions,
- *                                                      positions fastest in a tile
- * Context position i of sequence s lives at cache row kv_offsets[s] + i.  Every
- * kv_offsets[s] must be a multiple of 64 and kv_offsets[s+1] - kv_offsets[s] >= T_s
- * rounded up to a multiple of 64 (so 64-row tiles never leave a sequence's slot);
- * kv_cap is a multiple of 64 and >= kv_offsets[n_seq].  Rows past T_s inside a slot
- * are never used.  A 64-position tile of one head is thus 64*head_dim contiguous keys
- * and 64*head_dim contiguous values: the attention streams both as whole tiles. */
+/* KV cache, caller-owned, `dtype` elements, keys and values in two arrays of the same
+ * shape [n_layers][n_heads][kv_cap/64][64*head_dim]: the rows (positions) of one head
+ * are grouped in tiles of 64, and each tile holds its 64 x head_dim keys (values) in
+ * the order in which the attention kernel's 64 lanes take their matrix-core operands,
+ * so that every operand fetch is one contiguous 1 KB access.  With r the row inside
+ * the tile and i the dim:
+ *   keys:   ((st*(head_dim/32) + i/32)*64 + 16*((i/8)%4) + ql)*8 + i%8,
+ *           st = 2*(r/32) + (r/4)%2,  ql = 4*((r%32)/8) + r%4
+ *   values: (((r/32)*(head_dim/16) + i/16)*64 + 16*((r/8)%4) + i%16)*8 + r%8
+ * Keys are stored after RoPE.  Context position i of sequence s lives at cache row
+ * kv_offsets[s] + i.  Every kv_offsets[s] must be a multiple of 64 and
+ * kv_offsets[s+1] - kv_offsets[s] >= T_s rounded up to a multiple of 64 (so 64-row
+ * tiles never leave a sequence's slot); kv_cap is a multiple of 64 and
+ * >= kv_offsets[n_seq].  Rows past T_s inside a slot are never used. */
 size_t hdf_kv_cache_bytes(const hdf_drafter* w, int64_t kv_cap); /* bytes of k (= of vt) */
 
 /* Workspace bytes hdf_draft_block needs for these sizes (0 on invalid arguments). */

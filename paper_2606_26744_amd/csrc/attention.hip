@@ -4,10 +4,10 @@
 // the anchor and the context, Sec. 1 and Sec. 2.1).  Softmax scale 1/sqrt(hd),
 // fp32 softmax with online rescaling.
 //
-// Layouts (one layer): keys K[head][row][hd] (rows of a sequence contiguous),
-// values in 64-row tiles Vt[head][row/64][hd][64] (rows fastest inside a tile), so
-// a 64-key tile of one head is 16 KB of contiguous keys plus 16 KB of contiguous
-// values.  The context of sequence s starts at cache row kv_offsets[s] (a multiple
+// Layouts (one layer): keys and values of a head in 64-row tiles, each tile in the
+// operand order of the MFMA instructions below (kc_offset / vc_offset), so a 64-key
+// tile of one head is 16 KB of contiguous keys plus 16 KB of contiguous values and
+// every operand load is a contiguous 1 KB per wave.  The context of sequence s starts at cache row kv_offsets[s] (a multiple
 // of 64); its block keys sit in 64-row slot s of separate block buffers of the
 // same layout.
 //
@@ -19,8 +19,7 @@
 //                                      as a bf16 hi + lo pair
 // Keys inside each 32-key step are ordered so that the S^T accumulator a lane
 // holds (4 keys of one query per 16-key sub-tile) is exactly the 8 keys of one
-// query the P^T operand needs, so P never leaves registers; V^T operands are one
-// 16-byte load each from the transposed cache.  No LDS in the key loop.  The four
+// query the P^T operand needs, so P never leaves registers.  No LDS in the key loop.  The four
 // waves of a workgroup merge through LDS at the end; chunks merge in a combine
 // kernel (log-sum-exp rescaling).
 #include "common.hpp"
@@ -91,24 +90,22 @@ attn_bf16_kernel(AttnArgs a) {
 
   for (int t0 = k_lo + wid * kKeyTile; t0 < k_hi; t0 += kAttnWaves * kKeyTile) {
     // K operands of the four 16-key sub-tiles: sub-tile st = 2*ks + p, row r -> key
-    // t0 + 32ks + 8(r/4) + 4p + r%4.
+    // t0 + 32ks + 8(r/4) + 4p + r%4 (the order of the cache tile layout).
+    // In the cache tile layout each operand is 64 lanes x 16 contiguous bytes.
+    const bf16_t* ktile = kbase + int64_t(t0) * HD + lane * 8;
     bf16x8_t kf[4][NJ];
 #pragma unroll
-    for (int st = 0; st < 4; ++st) {
-      const int key = t0 + 32 * (st >> 1) + 8 * (ql >> 2) + 4 * (st & 1) + (ql & 3);
-      const bf16_t* krow = kbase + int64_t(key) * HD + 8 * g;
+    for (int st = 0; st < 4; ++st)
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) kf[st][j] = __builtin_bit_cast(bf16x8_t, ld16(krow + 32 * j));
-    }
-    // V^T operands: lane holds V^T[16dt + ql][t0 + 32ks + 8g .. +7], one 16-byte load
-    // from the tile of keys t0..t0+63.
-    const bf16_t* vtile = vbase + int64_t(t0 >> 6) * HD * 64;
+      for (int j = 0; j < NJ; ++j)
+        kf[st][j] = __builtin_bit_cast(bf16x8_t, ld16(ktile + (st * NJ + j) * 512));
+    // V^T operands: lane holds V^T[16dt + ql][t0 + 32ks + 8g .. +7].
+    const bf16_t* vtile = vbase + int64_t(t0 >> 6) * HD * 64 + lane * 8;
     u32x4 vf[2][NDT];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt)
-        vf[ks][dt] = ld16(vtile + (16 * dt + ql) * 64 + 32 * ks + 8 * g);
+      for (int dt = 0; dt < NDT; ++dt) vf[ks][dt] = ld16(vtile + (ks * NDT + dt) * 512);
 
     float sv[4][4];
 #pragma unroll
@@ -324,7 +321,7 @@ __global__ void attn_f32_kernel(AttnArgs a, float* __restrict__ out) {
     }
     for (int j = 0; j < n; ++j) {
       float sc = 0.f;
-      for (int i = 0; i < hd; ++i) sc = fmaf(Q[i], K[int64_t(j) * hd + i], sc);
+      for (int i = 0; i < hd; ++i) sc = fmaf(Q[i], K[kc_index(j, i, hd)], sc);
       sc *= scale;
       const float mn = fmaxf(m, sc);
       const float al = expf(m - mn);
@@ -332,7 +329,7 @@ __global__ void attn_f32_kernel(AttnArgs a, float* __restrict__ out) {
       l = l * al + p;
 #pragma unroll
       for (int i = 0; i < hd; ++i)
-        o[i] = o[i] * al + p * Vt[(int64_t(j >> 6) * hd + i) * 64 + (j & 63)];
+        o[i] = o[i] * al + p * Vt[vc_index(j, i, hd)];
       m = mn;
     }
   }

@@ -68,6 +68,35 @@ __device__ __forceinline__ void st_nt16(void* p, u32x4 v) {
   __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
 }
 
+// KV cache layout.  Rows (positions) of one head are grouped in tiles of 64, each
+// tile 64*hd contiguous elements in the order in which the attention kernel's 64
+// lanes take their matrix-core operands, so every operand load is one contiguous
+// 1 KB (bf16) access:
+//   keys   (S^T = K.Q^T, K the A operand of v_mfma_f32_16x16x32_bf16): row r of the
+//          tile is row ql = 4*((r%32)/8) + r%4 of 16-key sub-tile st = 2*(r/32) +
+//          (r/4)%2; dim i is k-slice j = i/32, lane group g = (i/8)%4, element i%8;
+//          offset ((st*(hd/32) + j)*64 + 16g + ql)*8 + i%8
+//   values (O^T += V^T.P^T, V^T the A operand): dim i is row ql = i%16 of 16-dim
+//          tile dt = i/16; row r is k-slice r/32, lane group (r/8)%4, element r%8;
+//          offset (((r/32)*(hd/16) + dt)*64 + 16*((r/8)%4) + ql)*8 + r%8
+__host__ __device__ __forceinline__ int64_t kc_offset(int r, int i, int hd) {
+  const int rr = r & 31;
+  const int st = 2 * (r >> 5) + ((rr >> 2) & 1);
+  const int ql = 4 * (rr >> 3) + (rr & 3);
+  return ((int64_t(st) * (hd >> 5) + (i >> 5)) * 64 + ((i >> 3) & 3) * 16 + ql) * 8 + (i & 7);
+}
+__host__ __device__ __forceinline__ int64_t vc_offset(int r, int i, int hd) {
+  return ((int64_t(r >> 5) * (hd >> 4) + (i >> 4)) * 64 + ((r >> 3) & 3) * 16 + (i & 15)) * 8 +
+         (r & 7);
+}
+// Element offset of (row, dim) in one head's keys / values (cap rows, cap % 64 == 0).
+__host__ __device__ __forceinline__ int64_t kc_index(int64_t row, int i, int hd) {
+  return (row >> 6) * 64 * hd + kc_offset(int(row & 63), i, hd);
+}
+__host__ __device__ __forceinline__ int64_t vc_index(int64_t row, int i, int hd) {
+  return (row >> 6) * 64 * hd + vc_offset(int(row & 63), i, hd);
+}
+
 // SiLU(g) * u, the gated MLP activation.
 __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.f + __expf(-g)) * u; }
 

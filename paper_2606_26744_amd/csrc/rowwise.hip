@@ -181,9 +181,8 @@ __device__ __forceinline__ void row_dest(const QkvEpiArgs& a, int r, int& pos, i
 
 // Projection epilogue of one tile of kQkvRows rows x one head: sums the split-K
 // partials, rotates (i, i+hd/2) pairs of Q and K at each row's position and stores
-// them row-major; V goes through LDS and is stored in 64-position tiles with
-// positions fastest ([head][row/64][hd][64]), so consecutive lanes store
-// consecutive positions.
+// Q row-major and K in the cache's tile layout; V goes through LDS so that
+// consecutive lanes store consecutive positions of one dim.
 constexpr int kQkvRows = 16;
 
 template <typename T, int HD>
@@ -236,13 +235,16 @@ qkv_epilogue_kernel(QkvEpiArgs a) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) rope_rotate(y1[j], y2[j], cv[j], sv[j]);
     }
-    T* dst;
-    if (part == 0)
-      dst = static_cast<T*>(a.q) + ((int64_t(s_s[rr]) * a.nh + h) * a.B + s_k[rr]) * HD;
-    else
-      dst = static_cast<T*>(a.k) + (int64_t(h) * a.cap + s_drow[rr]) * HD;
-    store4<T>(dst + i0, y1);
-    store4<T>(dst + i0 + HALF, y2);
+    if (part == 0) {
+      T* dst = static_cast<T*>(a.q) + ((int64_t(s_s[rr]) * a.nh + h) * a.B + s_k[rr]) * HD;
+      store4<T>(dst + i0, y1);
+      store4<T>(dst + i0 + HALF, y2);
+    } else {
+      // Four consecutive dims (i0 % 4 == 0) stay contiguous in the cache tile layout.
+      T* kh = static_cast<T*>(a.k) + int64_t(h) * a.cap * HD;
+      store4<T>(kh + kc_index(s_drow[rr], i0, HD), y1);
+      store4<T>(kh + kc_index(s_drow[rr], i0 + HALF, HD), y2);
+    }
   }
   // V part -> LDS.
   const int64_t vcol = int64_t(2 - a.first_part) * a.d + int64_t(h) * HD;
@@ -261,12 +263,11 @@ qkv_epilogue_kernel(QkvEpiArgs a) {
     vt_tile[rr][i0 + 3] = x.w;
   }
   __syncthreads();
-  T* vt = static_cast<T*>(a.vt) + int64_t(h) * (a.cap / 64) * HD * 64;
+  T* vt = static_cast<T*>(a.vt) + int64_t(h) * a.cap * HD;
   for (int e = threadIdx.x; e < rows * HD; e += kRowThreads) {
     const int i = e / rows;
     const int rr = e - i * rows;
-    const int64_t drow = s_drow[rr];
-    store1<T>(vt + ((drow >> 6) * HD + i) * 64 + (drow & 63), vt_tile[rr][i]);
+    store1<T>(vt + vc_index(s_drow[rr], i, HD), vt_tile[rr][i]);
   }
 }
 

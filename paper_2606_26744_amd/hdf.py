@@ -283,14 +283,13 @@ class DrafterHandle:
         return int(lib().hdf_draft_block_workspace(ctypes.byref(self.s), n_seq, B, n_new, max_ctx))
 
     def alloc_kv(self, kv_cap: int, device="cuda"):
-        """KV cache tensors in the library's layout: k [L][nh][cap][hd], vt
-        [L][nh][cap/64][hd][64] (values in 64-position tiles, positions fastest)."""
+        """KV cache tensors in the library's layout: keys and values each
+        [L][nh][cap/64][64*hd], 64-position tiles in matrix-core operand order."""
         if kv_cap % 64:
             raise ValueError("kv_cap must be a multiple of 64")
-        shape_k = (self.L, self.nh, kv_cap, self.hd)
-        shape_vt = (self.L, self.nh, kv_cap // 64, self.hd, 64)
-        return (torch.zeros(shape_k, dtype=self.torch_dtype, device=device),
-                torch.zeros(shape_vt, dtype=self.torch_dtype, device=device))
+        shape = (self.L, self.nh, kv_cap // 64, 64 * self.hd)
+        return (torch.zeros(shape, dtype=self.torch_dtype, device=device),
+                torch.zeros(shape, dtype=self.torch_dtype, device=device))
 
     def draft_block(self, *, ctx_len: torch.Tensor, max_ctx: int, y_new: torch.Tensor,
                     new_offsets: torch.Tensor, kv_offsets: torch.Tensor, kv_k: torch.Tensor,
@@ -298,7 +297,7 @@ class DrafterHandle:
                     ws: Optional[torch.Tensor] = None, stream=None):
         n_seq, B = tokens.shape
         n_new = y_new.shape[0]
-        kv_cap = kv_k.shape[2]
+        kv_cap = kv_k.shape[2] * 64
         dev = tokens.device
         if hidden is None:
             hidden = torch.empty((n_seq * B, self.d), dtype=self.torch_dtype, device=dev)
@@ -313,33 +312,63 @@ class DrafterHandle:
         return hidden
 
 
+_KV_PERM = {}
+
+
+def _kv_perm(hd: int, device):
+    """Offsets of (row r, dim i) inside a 64-row cache tile for keys and for values
+    (the library's tile layout, see hdf.h): two [64, hd] int64 tensors."""
+    key = (hd, str(device))
+    if key not in _KV_PERM:
+        r = torch.arange(64).view(64, 1)
+        i = torch.arange(hd).view(1, hd)
+        rr = r % 32
+        st = 2 * (r // 32) + (rr // 4) % 2
+        ql = 4 * (rr // 8) + rr % 4
+        k_off = ((st * (hd // 32) + i // 32) * 64 + ((i // 8) % 4) * 16 + ql) * 8 + i % 8
+        v_off = (((r // 32) * (hd // 16) + i // 16) * 64 + ((r // 8) % 4) * 16 + i % 16) * 8 + r % 8
+        _KV_PERM[key] = (k_off.to(device), v_off.to(device))
+    return _KV_PERM[key]
+
+
 def write_kv_rows(kv_k: torch.Tensor, kv_vt: torch.Tensor, layer: int, row0: int,
                   k_rows: torch.Tensor, v_rows: torch.Tensor):
     """Copies keys/values of consecutive positions [n, nh*hd] into cache rows row0..row0+n-1
-    (row0 a multiple of 64) of one layer.  Layout conversion only."""
+    (row0 a multiple of 64) of one layer.  Layout conversion only; the rest of the last
+    64-row tile is zero-filled."""
     n = k_rows.shape[0]
     if n == 0:
         return
-    _, nh, _, hd = kv_k.shape
+    _, nh, tiles, tsz = kv_k.shape
+    hd = tsz // 64
     if row0 % 64:
         raise ValueError("row0 must be a multiple of 64")
-    kv_k[layer, :, row0:row0 + n, :] = k_rows.view(n, nh, hd).permute(1, 0, 2)
     n64 = (n + 63) // 64
-    vp = torch.zeros((n64 * 64, nh, hd), dtype=v_rows.dtype, device=v_rows.device)
-    vp[:n] = v_rows.view(n, nh, hd)
     t0 = row0 // 64
-    kv_vt[layer, :, t0:t0 + n64] = vp.view(n64, 64, nh, hd).permute(2, 0, 3, 1)
+    k_off, v_off = _kv_perm(hd, kv_k.device)
+    for src, dst, off in ((k_rows, kv_k, k_off), (v_rows, kv_vt, v_off)):
+        rows = torch.zeros((n64 * 64, nh, hd), dtype=src.dtype, device=src.device)
+        rows[:n] = src.view(n, nh, hd)
+        t = rows.view(n64, 64, nh, hd).permute(2, 0, 1, 3).reshape(nh, n64, 64 * hd)
+        out = torch.empty_like(t)
+        out.scatter_(2, off.reshape(1, 1, -1).expand(nh, n64, -1), t)
+        dst[layer, :, t0:t0 + n64] = out
 
 
 def read_kv_rows(kv_k: torch.Tensor, kv_vt: torch.Tensor, layer: int, row0: int, n: int):
     """Keys/values of cache rows row0..row0+n-1 of one layer as [n, nh*hd] tensors."""
-    _, nh, _, hd = kv_k.shape
-    k = kv_k[layer, :, row0:row0 + n, :].permute(1, 0, 2).reshape(n, nh * hd)
+    _, nh, tiles, tsz = kv_k.shape
+    hd = tsz // 64
     t_lo, t_hi = row0 // 64, (row0 + n + 63) // 64
-    vt = kv_vt[layer, :, t_lo:t_hi]                       # [nh][tiles][hd][64]
-    v = vt.permute(1, 3, 0, 2).reshape((t_hi - t_lo) * 64, nh * hd)
-    off = row0 - t_lo * 64
-    return k.contiguous(), v[off:off + n].contiguous()
+    k_off, v_off = _kv_perm(hd, kv_k.device)
+    res = []
+    for src, off in ((kv_k, k_off), (kv_vt, v_off)):
+        t = src[layer, :, t_lo:t_hi]                                   # [nh][tiles][64*hd]
+        g = torch.gather(t, 2, off.reshape(1, 1, -1).expand(nh, t_hi - t_lo, -1))
+        rows = g.view(nh, t_hi - t_lo, 64, hd).permute(1, 2, 0, 3).reshape((t_hi - t_lo) * 64, nh * hd)
+        off0 = row0 - t_lo * 64
+        res.append(rows[off0:off0 + n].contiguous())
+    return res[0], res[1]
 
 
 def kv_slot_offsets(ctx_lens: Sequence[int]) -> list:

@@ -96,3 +96,24 @@ def test_pack_weight_validation():
     assert _status(L.hdf_pack_weight(fake, fake, 70, 48, 1, None)) == "HDF_E_INVALID"   # in place
     assert _status(L.hdf_pack_weight(fake, ctypes.c_void_p(8192), 70, 40, 1, None)) == "HDF_E_INVALID"
     assert _status(L.hdf_pack_weight(fake, ctypes.c_void_p(8192), 70, 48, 5, None)) == "HDF_E_INVALID"
+
+
+def test_kv_tile_layout_roundtrip():
+    """The cache tile layout is a permutation of each 64-row tile, and writing rows then
+    reading them back returns them (keys and values), for both head widths."""
+    import torch
+    for hd in (64, 128):
+        k_off, v_off = hdf._kv_perm(hd, "cpu")
+        for off in (k_off, v_off):
+            assert torch.equal(torch.sort(off.reshape(-1)).values, torch.arange(64 * hd))
+        nh, n, row0 = 3, 100, 64
+        kv_k = torch.zeros((1, nh, 4, 64 * hd))
+        kv_vt = torch.zeros((1, nh, 4, 64 * hd))
+        k = torch.randn(n, nh * hd)
+        v = torch.randn(n, nh * hd)
+        hdf.write_kv_rows(kv_k, kv_vt, 0, row0, k, v)
+        k2, v2 = hdf.read_kv_rows(kv_k, kv_vt, 0, row0, n)
+        assert torch.equal(k2, k) and torch.equal(v2, v)
+        # key (row r, dim i) of head h sits at kv_k[0, h, tile, k_off[r, i]]
+        assert kv_k[0, 1, 1, k_off[5, 7]] == k[5, hd + 7]
+        assert kv_vt[0, 2, 2, v_off[3, hd - 1]] == v[64 + 3, 2 * hd + hd - 1]
