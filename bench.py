@@ -26,10 +26,10 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 # HBM bytes per LM-head launch from the two rocprofv3 --pmc runs recorded in
-# profiles/lm_head_argmax_hbm_counters.md (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0, the
-# factors a plain 2 GiB device copy gives).  Valid only for the kernel source it was
-# measured on: reported as null once gemm.hip or common.hpp changes.
-LM_HEAD_TRAFFIC = {"source_sha": "172fec464fbd5aa2", "bytes": (533587.2 * 2.0 + 1010.0 * 1.0) * 1024}
+# profiles/lm_head_argmax_hbm_counters.md (FETCH_SIZE x 2.049 + WRITE_SIZE x 1.025, the
+# factors a plain device copy of known size gives).  Valid only for the kernel source it
+# was measured on: reported as null once gemm.hip or common.hpp changes.
+LM_HEAD_TRAFFIC = {"source_sha": "14dabffda2abc6c9", "bytes": (531981.3 * 2.049 + 505.0 * 1.025) * 1024}
 BF16_PEAK_TFLOPS = 2500.0
 METRIC = "draft blocks/sec at d=4096,B=16,V=129280; reducer HBM GB/s; MFMA util %"
 
