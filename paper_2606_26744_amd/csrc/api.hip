@@ -113,6 +113,12 @@ DraftPlan plan_workspace(const hdf_drafter& w, int n_seq, int B, int64_t n_new, 
   };
   upd(crow, 2 * w.d, w.d);
   upd(n_new % kCtxChunk, 2 * w.d, w.d);  // a shorter last chunk may split further
+  if (bf && n_new > 0 && n_new <= kCtxChunk) {
+    // Context K/V and block QKV in one launch: both problems' partials.
+    const size_t sp = size_t(hdf::gemm_plan2(bf, int(n_new), 2 * w.d, int(M), 3 * w.d, w.d).splits);
+    const size_t b = sp * (size_t(n_new) * 2 * w.d + M * 3 * w.d) * 4;
+    if (b > parts) parts = b;
+  }
   upd(int64_t(M), 3 * w.d, w.d);
   upd(int64_t(M), w.d, w.d);
   upd(int64_t(M), 2 * w.d_ff, w.d);
@@ -301,42 +307,62 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
     pa.d = d; pa.eps = w->eps;
     return hdf::launch_prep(bf, pa, s);
   };
-  // Context rows projected in this call, in chunks: K/V of every layer into the cache.
+  auto ctx_epi = [&](int l, int64_t r0, int rows, int S, const float* pp) {
+    hdf::QkvEpiArgs ea{};
+    ea.parts = pp; ea.S = S; ea.M = rows; ea.first_part = 1;
+    ea.d = d; ea.nh = nh; ea.hd = hd; ea.B = B;
+    ea.ctx_len = ctx_len; ea.plan_pos = plan_pos + r0; ea.plan_row = plan_row + r0;
+    ea.rope_cs = w->rope_cs;
+    ea.q = nullptr;
+    ea.k = static_cast<char*>(kv_k) + l * layer_kv;
+    ea.vt = static_cast<char*>(kv_vt) + l * layer_kv;
+    ea.cap = kv_cap;
+    return ea;
+  };
+  auto blk_epi = [&](int S, const float* pp) {
+    hdf::QkvEpiArgs ea{};
+    ea.parts = pp; ea.S = S; ea.M = M; ea.first_part = 0;
+    ea.d = d; ea.nh = nh; ea.hd = hd; ea.B = B;
+    ea.ctx_len = ctx_len; ea.rope_cs = w->rope_cs;
+    ea.q = q; ea.k = kb; ea.vt = vtb; ea.cap = capb;
+    return ea;
+  };
+  // Context rows projected in this call: with a bf16 drafter and at most one chunk of
+  // them, each layer's context K/V share one GEMM launch and one epilogue launch with
+  // the block's Q/K/V (below); otherwise K/V of every layer go into the cache here, in
+  // chunks of kCtxChunk rows.
+  const bool grouped = bf && n_new > 0 && n_new <= kCtxChunk;
   if (n_new == 0) HDF_TRY(prep(0, 0, true));
-  for (int64_t r0 = 0; r0 < n_new; r0 += kCtxChunk) {
+  if (grouped) HDF_TRY(prep(0, int(n_new), true));
+  for (int64_t r0 = 0; !grouped && r0 < n_new; r0 += kCtxChunk) {
     const int rows = int(n_new - r0 < kCtxChunk ? n_new - r0 : kCtxChunk);
     HDF_TRY(prep(r0, rows, r0 == 0));
     for (int l = 0; l < L; ++l) {
       // Rows d..3d-1 (W_k; W_v) of the packed W_qkv: d/128 whole row groups in.
       const char* wkv = static_cast<const char*>(w->w_qkv[l]) + size_t(d) * d * el;
       const hdf::GemmPlan Sp = hdf::gemm_plan(bf, rows, 2 * d, d);
-    const int S = Sp.splits;
       HDF_TRY(hdf::launch_gemm_partial(bf, cbuf, d, wkv, rows, 2 * d, d, Sp, parts, s));
-      hdf::QkvEpiArgs ea{};
-      ea.parts = parts; ea.S = S; ea.M = rows; ea.first_part = 1;
-      ea.d = d; ea.nh = nh; ea.hd = hd; ea.B = B;
-      ea.ctx_len = ctx_len; ea.plan_pos = plan_pos + r0; ea.plan_row = plan_row + r0;
-      ea.rope_cs = w->rope_cs;
-      ea.q = nullptr;
-      ea.k = static_cast<char*>(kv_k) + l * layer_kv;
-      ea.vt = static_cast<char*>(kv_vt) + l * layer_kv;
-      ea.cap = kv_cap;
-      HDF_TRY(hdf::launch_qkv_epilogue(bf, ea, s));
+      HDF_TRY(hdf::launch_qkv_epilogue(bf, ctx_epi(l, r0, rows, Sp.splits, parts), s));
     }
   }
 
   const int n_chunks = (max_ctx + P.chunk_len - 1) / P.chunk_len;
   for (int l = 0; l < L; ++l) {
-    // Q, K_b, V_b with RoPE at T_s + k.
-    const hdf::GemmPlan Sqp = hdf::gemm_plan(bf, M, 3 * d, d);
-    const int Sq = Sqp.splits;
-    HDF_TRY(hdf::launch_gemm_partial(bf, u, d, w->w_qkv[l], M, 3 * d, d, Sqp, parts, s));
-    hdf::QkvEpiArgs ea{};
-    ea.parts = parts; ea.S = Sq; ea.M = M; ea.first_part = 0;
-    ea.d = d; ea.nh = nh; ea.hd = hd; ea.B = B;
-    ea.ctx_len = ctx_len; ea.rope_cs = w->rope_cs;
-    ea.q = q; ea.k = kb; ea.vt = vtb; ea.cap = capb;
-    HDF_TRY(hdf::launch_qkv_epilogue(bf, ea, s));
+    // Q, K_b, V_b with RoPE at T_s + k (and the context rows' K/V when grouped).
+    if (grouped) {
+      const char* wkv = static_cast<const char*>(w->w_qkv[l]) + size_t(d) * d * el;
+      const int rows = int(n_new);
+      const hdf::GemmPlan Sg = hdf::gemm_plan2(bf, rows, 2 * d, M, 3 * d, d);
+      float* parts_blk = parts + size_t(Sg.splits) * rows * 2 * d;
+      HDF_TRY(hdf::launch_gemm_partial2(cbuf, d, wkv, rows, 2 * d, parts, u, d, w->w_qkv[l], M,
+                                        3 * d, parts_blk, d, Sg, s));
+      HDF_TRY(hdf::launch_qkv_epilogue2(bf, ctx_epi(l, 0, rows, Sg.splits, parts),
+                                        blk_epi(Sg.splits, parts_blk), s));
+    } else {
+      const hdf::GemmPlan Sqp = hdf::gemm_plan(bf, M, 3 * d, d);
+      HDF_TRY(hdf::launch_gemm_partial(bf, u, d, w->w_qkv[l], M, 3 * d, d, Sqp, parts, s));
+      HDF_TRY(hdf::launch_qkv_epilogue(bf, blk_epi(Sqp.splits, parts), s));
+    }
 
     hdf::AttnArgs aa{};
     aa.q = q;

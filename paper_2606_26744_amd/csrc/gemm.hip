@@ -76,9 +76,20 @@ gemm_bf16_kernel(GemmArgs p) {
   const int lane = tid & 63;
   const int wid = tid >> 6;
 
+  // Tiles of the first problem, then those of the optional second one.
+  const int tiles1 = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
+  int tile = remap_tile(blockIdx.x, gridDim.x);
+  const bool second = tile >= tiles1;
+  if (second) {
+    tile -= tiles1;
+    p.A = p.A2;
+    p.lda = p.lda2;
+    p.B = p.B2;
+    p.M = p.M2;
+    p.N = p.N2;
+    p.C = p.C2;
+  }
   const int mt = (p.M + BM - 1) / BM;
-  const int nt = (p.N + BN - 1) / BN;
-  const int tile = remap_tile(blockIdx.x, mt * nt);
   const int n_tile = tile / mt, m_tile = tile % mt;
   const int m0 = m_tile * BM, n0 = n_tile * BN;
 
@@ -368,8 +379,9 @@ constexpr int kArgmaxWaves = 8;
 
 template <int NW>
 static void launch_bf16_partial(const GemmArgs& a, int splits, hipStream_t s) {
-  const int BM = a.M <= 64 ? 64 : 128;
-  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + 32 * NW - 1) / (32 * NW));
+  const int BM = (a.M <= 64 && a.M2 <= 64) ? 64 : 128;
+  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + 32 * NW - 1) / (32 * NW)) +
+                    ((a.M2 + BM - 1) / BM) * ((a.N2 + 32 * NW - 1) / (32 * NW));
   const dim3 grid(tiles, 1, splits), block(NW * 64);
   if (BM == 64)
     hipLaunchKernelGGL((gemm_bf16_kernel<64, NW, 4, kEpiPartial>), grid, block, 0, s, a);
@@ -407,7 +419,9 @@ static hipError_t launch_gemm_any(bool bf16, int epi, const GemmArgs& a, GemmPla
 
 int gemm_k_align(bool bf16) { return bf16 ? kBK : 16; }
 
-GemmPlan gemm_plan(bool bf16, int M, int N, int K) {
+GemmPlan gemm_plan(bool bf16, int M, int N, int K) { return gemm_plan2(bf16, M, N, 0, 0, K); }
+
+GemmPlan gemm_plan2(bool bf16, int M, int N, int M2, int N2, int K) {
   const int ncu = device_cu_count();
   const int nk = K / gemm_k_align(bf16);
   if (!bf16) {
@@ -423,12 +437,12 @@ GemmPlan gemm_plan(bool bf16, int M, int N, int K) {
   // the CUs best without exceeding them; ties go to fewer splits (less partial
   // traffic) and then to more waves (more bytes in flight per CU).  Every split keeps
   // at least 8 K-steps.
-  const int BM = M <= 64 ? 64 : 128;
-  const int mt = (M + BM - 1) / BM;
+  const int BM = (M <= 64 && M2 <= 64) ? 64 : 128;
   GemmPlan best{4, 1};
   double best_fill = -1.0;
   for (int nw : {4, 6, 8}) {
-    const int tiles = mt * ((N + 32 * nw - 1) / (32 * nw));
+    const int tiles = ((M + BM - 1) / BM) * ((N + 32 * nw - 1) / (32 * nw)) +
+                      ((M2 + BM - 1) / BM) * ((N2 + 32 * nw - 1) / (32 * nw));
     for (int s = 1; s <= 16; ++s) {
       if (s > 1 && nk / s < 8) break;
       const int wgs = tiles * s;
@@ -469,6 +483,16 @@ hipError_t launch_gemm_partial(bool bf16, const void* A, int64_t lda, const void
   a.A = A; a.lda = lda; a.B = B;
   a.M = M; a.N = N; a.K = K; a.C = C; a.keys = nullptr;
   return launch_gemm_any(bf16, kEpiPartial, a, plan, s);
+}
+
+hipError_t launch_gemm_partial2(const void* A, int64_t lda, const void* B, int M, int N,
+                                float* C, const void* A2, int64_t lda2, const void* B2, int M2,
+                                int N2, float* C2, int K, GemmPlan plan, hipStream_t s) {
+  GemmArgs a{};
+  a.A = A; a.lda = lda; a.B = B;
+  a.M = M; a.N = N; a.K = K; a.C = C; a.keys = nullptr;
+  a.A2 = A2; a.lda2 = lda2; a.B2 = B2; a.M2 = M2; a.N2 = N2; a.C2 = C2;
+  return launch_gemm_any(true, kEpiPartial, a, plan, s);
 }
 
 hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t M, int d, int V,

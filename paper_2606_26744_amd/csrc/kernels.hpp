@@ -35,6 +35,13 @@ struct GemmArgs {
   int M, N, K;
   float* C;
   unsigned long long* keys;
+  // Optional second problem of the same K in the same launch (partial GEMMs only):
+  // its tiles follow the first problem's; C2[z][M2][N2].
+  const void* A2;
+  int64_t lda2;
+  const void* B2;
+  int M2, N2;
+  float* C2;
 };
 
 int gemm_k_align(bool bf16);                       // K must be a multiple of this
@@ -44,11 +51,17 @@ struct GemmPlan {
   int nw, splits;
 };
 GemmPlan gemm_plan(bool bf16, int M, int N, int K);
+// Plan of two problems of the same K launched together (M2 = 0: one problem).
+GemmPlan gemm_plan2(bool bf16, int M, int N, int M2, int N2, int K);
 size_t packed_weight_elems(int N, int K);          // rows rounded up to 128
 hipError_t launch_pack_weight(bool bf16, const void* src, void* dst, int N, int K, hipStream_t s);
 // C[z][M][N] (fp32) = A[M][K] . W[N][K]^T over the z-th of `splits` K ranges; W packed.
 hipError_t launch_gemm_partial(bool bf16, const void* A, int64_t lda, const void* B, int M, int N,
                                int K, GemmPlan plan, float* C, hipStream_t s);
+// Two bf16 problems of the same K in one launch (one wave of workgroups for both).
+hipError_t launch_gemm_partial2(const void* A, int64_t lda, const void* B, int M, int N,
+                                float* C, const void* A2, int64_t lda2, const void* B2, int M2,
+                                int N2, float* C2, int K, GemmPlan plan, hipStream_t s);
 // keys: M 64-bit scratch words.  logits may be NULL.
 hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t M, int d, int V,
                           unsigned long long* keys, int32_t* argmax, float* max_logit,
@@ -98,6 +111,9 @@ hipError_t launch_prep(bool bf16, const PrepArgs& a, hipStream_t s);
 hipError_t launch_residual_norm(bool bf16, const float* parts, int S, const float* gamma, float eps,
                                 int64_t rows, int d, float* h, void* u, hipStream_t s);
 hipError_t launch_qkv_epilogue(bool bf16, const QkvEpiArgs& a, hipStream_t s);
+// Two epilogues (context rows, block rows) in one launch.
+hipError_t launch_qkv_epilogue2(bool bf16, const QkvEpiArgs& a, const QkvEpiArgs& b,
+                                hipStream_t s);
 // act = SiLU(gate) * up from parts [S][M][2F] (gate columns first)
 hipError_t launch_silu_epilogue(bool bf16, const float* parts, int S, int64_t M, int F, void* act,
                                 hipStream_t s);

@@ -187,12 +187,15 @@ constexpr int kQkvRows = 16;
 
 template <typename T, int HD>
 __global__ void __launch_bounds__(kRowThreads)
-qkv_epilogue_kernel(QkvEpiArgs a) {
+qkv_epilogue_kernel(QkvEpiArgs a0, QkvEpiArgs a1, int nb0) {
   constexpr int HALF = HD / 2;
   __shared__ float vt_tile[kQkvRows][HD + 1];
   __shared__ int s_pos[kQkvRows], s_s[kQkvRows], s_k[kQkvRows];
   __shared__ int64_t s_drow[kQkvRows];
-  const int r0 = blockIdx.x * kQkvRows;
+  // Row tiles of the first set of rows, then of the optional second one.
+  const bool second = int(blockIdx.x) >= nb0;
+  const QkvEpiArgs a = second ? a1 : a0;
+  const int r0 = (second ? int(blockIdx.x) - nb0 : int(blockIdx.x)) * kQkvRows;
   const int h = blockIdx.y;
   const int rows = min(kQkvRows, a.M - r0);
   const int ncol = (3 - a.first_part) * a.d;
@@ -319,21 +322,31 @@ hipError_t launch_residual_norm(bool bf16, const float* parts, int S, const floa
   return hipGetLastError();
 }
 
-hipError_t launch_qkv_epilogue(bool bf16, const QkvEpiArgs& a, hipStream_t s) {
-  if (a.M <= 0) return hipSuccess;
-  const dim3 grid(unsigned((a.M + kQkvRows - 1) / kQkvRows), unsigned(a.nh));
+hipError_t launch_qkv_epilogue2(bool bf16, const QkvEpiArgs& a, const QkvEpiArgs& b,
+                                hipStream_t s) {
+  const int nb0 = a.M > 0 ? (a.M + kQkvRows - 1) / kQkvRows : 0;
+  const int nb1 = b.M > 0 ? (b.M + kQkvRows - 1) / kQkvRows : 0;
+  if (nb0 + nb1 == 0) return hipSuccess;
+  const int nh = nb0 > 0 ? a.nh : b.nh, hd = nb0 > 0 ? a.hd : b.hd;
+  const dim3 grid(unsigned(nb0 + nb1), unsigned(nh));
   if (bf16) {
-    if (a.hd == 128)
-      hipLaunchKernelGGL((qkv_epilogue_kernel<bf16_t, 128>), grid, dim3(kRowThreads), 0, s, a);
+    if (hd == 128)
+      hipLaunchKernelGGL((qkv_epilogue_kernel<bf16_t, 128>), grid, dim3(kRowThreads), 0, s, a, b, nb0);
     else
-      hipLaunchKernelGGL((qkv_epilogue_kernel<bf16_t, 64>), grid, dim3(kRowThreads), 0, s, a);
+      hipLaunchKernelGGL((qkv_epilogue_kernel<bf16_t, 64>), grid, dim3(kRowThreads), 0, s, a, b, nb0);
   } else {
-    if (a.hd == 128)
-      hipLaunchKernelGGL((qkv_epilogue_kernel<float, 128>), grid, dim3(kRowThreads), 0, s, a);
+    if (hd == 128)
+      hipLaunchKernelGGL((qkv_epilogue_kernel<float, 128>), grid, dim3(kRowThreads), 0, s, a, b, nb0);
     else
-      hipLaunchKernelGGL((qkv_epilogue_kernel<float, 64>), grid, dim3(kRowThreads), 0, s, a);
+      hipLaunchKernelGGL((qkv_epilogue_kernel<float, 64>), grid, dim3(kRowThreads), 0, s, a, b, nb0);
   }
   return hipGetLastError();
+}
+
+hipError_t launch_qkv_epilogue(bool bf16, const QkvEpiArgs& a, hipStream_t s) {
+  QkvEpiArgs none = a;
+  none.M = 0;
+  return launch_qkv_epilogue2(bf16, a, none, s);
 }
 
 hipError_t launch_silu_epilogue(bool bf16, const float* parts, int S, int64_t M, int F, void* act,
