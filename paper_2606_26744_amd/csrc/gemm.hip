@@ -53,17 +53,22 @@ __device__ __forceinline__ unsigned long long argmax_key(float v, int col) {
          static_cast<unsigned long long>(0xFFFFFFFFu - static_cast<uint32_t>(col));
 }
 
-template <int BM, int NW, int STAGES, int EPI>
+// TN: 32-column weight blocks per wave (1 or 2).  Each activation fragment read from
+// LDS feeds TN matrix-core operations, so TN = 2 halves the LDS traffic per MFMA; the
+// compute-bound shapes (a few hundred rows and more) need it, the weight streams of
+// 128 rows prefer more waves per CU instead.
+template <int BM, int NW, int STAGES, int EPI, int TN = 1>
 __global__ void __launch_bounds__(NW * 64)
 gemm_bf16_kernel(GemmArgs p) {
   constexpr int THREADS = NW * 64;
   constexpr int TM = BM / 32;
-  constexpr int BN = 32 * NW;                     // NW waves x 32 columns
+  constexpr int NB = NW * TN;                     // 32-column blocks of a tile
+  constexpr int BN = 32 * NB;
   constexpr int LDA = kBK + 8;                    // padded LDS row (bf16 elements)
   constexpr int A_CHUNKS = BM * kBK / 8;           // 16-byte chunks of an activation step
   constexpr int A_CH = (A_CHUNKS + THREADS - 1) / THREADS;
   constexpr int LDC = 33;                         // padded row of a wave's 32 columns
-  static_assert(EPI != kEpiArgmax || NW % 4 == 0, "argmax tiles are whole 4-wave slabs");
+  static_assert(EPI != kEpiArgmax || NB % 4 == 0, "argmax tiles are whole 128-column slabs");
   // LDS: the double-buffered activation tile, reused after the K loop by the ARGMAX
   // epilogue to stage the fp32 tile of four waves at a time ([wave][row][32 columns]).
   constexpr size_t kMainLds = size_t(2) * BM * LDA * sizeof(bf16_t);
@@ -100,24 +105,31 @@ gemm_bf16_kernel(GemmArgs p) {
   const int nk = kt_end - kt_begin;
 
   const bf16_t* A = static_cast<const bf16_t*>(p.A);
-  // This wave's 32-row weight block: block b = n_tile*NW + wid is sub-block b%4 of
-  // 128-row group b/4 (rows past N are zero padding of the packed layout; a group past
-  // the last one is clamped to it, and the columns it computes are never stored).
+  // This wave's 32-row weight blocks: block b = n_tile*NB + wid*TN + tn is sub-block
+  // b%4 of 128-row group b/4 (rows past N are zero padding of the packed layout; a
+  // group past the last one is clamped to it, and the columns it computes are never
+  // stored).
   const int n_groups = (p.N + 127) >> 7;
-  const int blk = n_tile * NW + wid;
-  const int grp = min(blk >> 2, n_groups - 1);
-  const bf16_t* Bw = static_cast<const bf16_t*>(p.B) +
-                     (int64_t(grp) * (p.K >> 4) * 4 + (blk & 3)) * 512 + lane * 8;
+  const bf16_t* Bw[TN];
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) {
+    const int blk = n_tile * NB + wid * TN + tn;
+    const int grp = min(blk >> 2, n_groups - 1);
+    Bw[tn] = static_cast<const bf16_t*>(p.B) +
+             (int64_t(grp) * (p.K >> 4) * 4 + (blk & 3)) * 512 + lane * 8;
+  }
 
-  f32x16_t acc[TM];
+  f32x16_t acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
+    for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][tn][r] = 0.f;
 
   if (nk > 0) {
     u32x4 ra[STAGES][A_CH];
-    u32x4 rb[STAGES][4];
+    u32x4 rb[STAGES][TN * 4];
     // Activation chunk c of a K-step: row c/8, 16-byte column c%8.  Rows past M are
     // clamped (their products are never stored); loads stay unpredicated so the
     // compiler's outstanding-load counting is exact.
@@ -133,7 +145,9 @@ gemm_bf16_kernel(GemmArgs p) {
     auto load_b = [&](int kt, u32x4* dst) {
       const int64_t kb = int64_t(kt_begin + min(kt, nk - 1)) * (kBK / 16);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) dst[q] = ld_nt16(Bw + (kb + q) * 4 * 512);
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) dst[q * TN + tn] = ld_nt16(Bw[tn] + (kb + q) * 4 * 512);
     };
     auto store_a = [&](const u32x4* src, int buf) {
 #pragma unroll
@@ -147,12 +161,14 @@ gemm_bf16_kernel(GemmArgs p) {
     auto compute = [&](int buf, const u32x4* bq) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const bf16x8_t bf = __builtin_bit_cast(bf16x8_t, bq[q]);
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
           const bf16x8_t af =
               *reinterpret_cast<const bf16x8_t*>(&As[buf][arow + 32 * i][q * 16 + kof]);
-          acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bf, acc[i], 0, 0, 0);
+#pragma unroll
+          for (int tn = 0; tn < TN; ++tn)
+            acc[i][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                af, __builtin_bit_cast(bf16x8_t, bq[q * TN + tn]), acc[i][tn], 0, 0, 0);
         }
       }
     };
@@ -186,16 +202,19 @@ gemm_bf16_kernel(GemmArgs p) {
       if (kt + u < nk) step(kt + u, u);
   }
 
-  const int col = n0 + 32 * wid + (lane & 31);
   if constexpr (EPI == kEpiPartial) {
     float* C = p.C + int64_t(z) * p.M * p.N;
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int tn = 0; tn < TN; ++tn) {
+      const int col = n0 + 32 * (wid * TN + tn) + (lane & 31);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (row < p.M && col < p.N) C[int64_t(row) * p.N + col] = acc[i][r];
-      }
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (row < p.M && col < p.N) C[int64_t(row) * p.N + col] = acc[i][tn][r];
+        }
+    }
   } else {
     // Stage the fp32 tile in LDS, four waves (128 columns) at a time ([wave][row][column
     // of the wave]); THREADS/BM threads per row scan each 128-column slab (lowest column
@@ -208,16 +227,20 @@ gemm_bf16_kernel(GemmArgs p) {
     float best = -INFINITY;
     int bcol = 0x7FFFFFFF;
 #pragma unroll
-    for (int slab = 0; slab < NW / 4; ++slab) {
+    for (int slab = 0; slab < NB / 4; ++slab) {
       if (slab > 0) __syncthreads();
-      if ((wid >> 2) == slab) {
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+      for (int tn = 0; tn < TN; ++tn) {
+        const int b = wid * TN + tn;            // this wave's block inside the tile
+        if ((b >> 2) == slab) {
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int rr = 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-            Cs[((wid & 3) * BM + rr) * LDC + (lane & 31)] = acc[i][r];
-          }
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int rr = 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+              Cs[((b & 3) * BM + rr) * LDC + (lane & 31)] = acc[i][tn][r];
+            }
+        }
       }
       __syncthreads();
       const int c0 = n0 + 128 * slab;
@@ -375,35 +398,50 @@ __global__ void pack_weight_kernel(const T* __restrict__ src, T* __restrict__ ds
 
 // ---------------------------------------------------------------------------- host side
 
-constexpr int kArgmaxWaves = 8;
-
-template <int NW>
+template <int NW, int TN, int STAGES = 4>
 static void launch_bf16_partial(const GemmArgs& a, int splits, hipStream_t s) {
   const int BM = (a.M <= 64 && a.M2 <= 64) ? 64 : 128;
-  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + 32 * NW - 1) / (32 * NW)) +
-                    ((a.M2 + BM - 1) / BM) * ((a.N2 + 32 * NW - 1) / (32 * NW));
+  constexpr int BN = 32 * NW * TN;
+  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN) +
+                    ((a.M2 + BM - 1) / BM) * ((a.N2 + BN - 1) / BN);
   const dim3 grid(tiles, 1, splits), block(NW * 64);
   if (BM == 64)
-    hipLaunchKernelGGL((gemm_bf16_kernel<64, NW, 4, kEpiPartial>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<64, NW, STAGES, kEpiPartial, TN>), grid, block, 0, s, a);
   else
-    hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, 4, kEpiPartial>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, STAGES, kEpiPartial, TN>), grid, block, 0, s, a);
+}
+
+template <int NW, int TN, int STAGES>
+static void launch_bf16_argmax(const GemmArgs& a, hipStream_t s) {
+  const int BM = a.M <= 64 ? 64 : 128;
+  constexpr int BN = 32 * NW * TN;
+  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  const dim3 grid(tiles, 1, 1), block(NW * 64);
+  if (BM == 64)
+    hipLaunchKernelGGL((gemm_bf16_kernel<64, NW, STAGES, kEpiArgmax, TN>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, STAGES, kEpiArgmax, TN>), grid, block, 0, s, a);
 }
 
 static hipError_t launch_gemm_any(bool bf16, int epi, const GemmArgs& a, GemmPlan plan,
                                   hipStream_t s) {
   if (bf16) {
     if (epi == kEpiPartial) {
-      if (plan.nw == 8) launch_bf16_partial<8>(a, plan.splits, s);
-      else if (plan.nw == 6) launch_bf16_partial<6>(a, plan.splits, s);
-      else launch_bf16_partial<4>(a, plan.splits, s);
+      if (plan.tn == 2) {
+        launch_bf16_partial<8, 2, 2>(a, plan.splits, s);
+      } else if (plan.nw == 8) {
+        launch_bf16_partial<8, 1>(a, plan.splits, s);
+      } else if (plan.nw == 6) {
+        launch_bf16_partial<6, 1>(a, plan.splits, s);
+      } else {
+        launch_bf16_partial<4, 1>(a, plan.splits, s);
+      }
     } else {
-      const int BM = a.M <= 64 ? 64 : 128;
-      const int tiles = ((a.M + BM - 1) / BM) * ((a.N + 32 * kArgmaxWaves - 1) / (32 * kArgmaxWaves));
-      const dim3 grid(tiles, 1, 1), block(kArgmaxWaves * 64);
-      if (BM == 64)
-        hipLaunchKernelGGL((gemm_bf16_kernel<64, kArgmaxWaves, 2, kEpiArgmax>), grid, block, 0, s, a);
-      else
-        hipLaunchKernelGGL((gemm_bf16_kernel<128, kArgmaxWaves, 2, kEpiArgmax>), grid, block, 0, s, a);
+      if (plan.tn == 2) {
+        launch_bf16_argmax<8, 2, 2>(a, s);
+      } else {
+        launch_bf16_argmax<8, 1, 2>(a, s);
+      }
     }
     return hipGetLastError();
   }
@@ -437,12 +475,19 @@ GemmPlan gemm_plan2(bool bf16, int M, int N, int M2, int N2, int K) {
   // the CUs best without exceeding them; ties go to fewer splits (less partial
   // traffic) and then to more waves (more bytes in flight per CU).  Every split keeps
   // at least 8 K-steps.
+  // Above 128 rows the products are matrix-core bound: waves then own two column blocks
+  // each, which halves the LDS traffic per MFMA (measured at M = 1024: down 90 -> 85 us,
+  // the cold context projection 1182 -> 950 us).
   const int BM = (M <= 64 && M2 <= 64) ? 64 : 128;
-  GemmPlan best{4, 1};
+  const bool mfma_bound = M > 128 || M2 > 128;
+  const int tn = mfma_bound ? 2 : 1;
+  GemmPlan best{4, 1, tn};
   double best_fill = -1.0;
   for (int nw : {4, 6, 8}) {
-    const int tiles = ((M + BM - 1) / BM) * ((N + 32 * nw - 1) / (32 * nw)) +
-                      ((M2 + BM - 1) / BM) * ((N2 + 32 * nw - 1) / (32 * nw));
+    if (mfma_bound && nw != 8) continue;   // 8 waves x 2 blocks, a 2-step ring
+    const int bn = 32 * nw * tn;
+    const int tiles = ((M + BM - 1) / BM) * ((N + bn - 1) / bn) +
+                      ((M2 + BM - 1) / BM) * ((N2 + bn - 1) / bn);
     for (int s = 1; s <= 16; ++s) {
       if (s > 1 && nk / s < 8) break;
       const int wgs = tiles * s;
@@ -454,7 +499,7 @@ GemmPlan gemm_plan2(bool bf16, int M, int N, int M2, int N2, int K) {
       if (score > best_fill + 1e-9 ||
           (tie && (s < best.splits || (s == best.splits && nw > best.nw)))) {
         best_fill = score;
-        best = GemmPlan{nw, s};
+        best = GemmPlan{nw, s, tn};
       }
     }
   }
@@ -495,6 +540,13 @@ hipError_t launch_gemm_partial2(const void* A, int64_t lda, const void* B, int M
   return launch_gemm_any(true, kEpiPartial, a, plan, s);
 }
 
+GemmPlan lm_head_plan(int64_t M) {
+  // 128 rows and fewer: a weight stream, 8 waves of one block each (bytes in flight);
+  // more rows: matrix-core bound, 8 waves of two blocks each (half the LDS traffic per
+  // MFMA; M = 1024: 914 -> 848 us).
+  return M <= 128 ? GemmPlan{8, 1, 1} : GemmPlan{8, 1, 2};
+}
+
 hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t M, int d, int V,
                           unsigned long long* keys, int32_t* argmax, float* max_logit,
                           float* logits, hipStream_t s) {
@@ -513,7 +565,7 @@ hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t 
     a.M = rows; a.N = V; a.K = d;
     a.C = logits != nullptr ? logits + r0 * V : nullptr;
     a.keys = keys + r0;
-    e = launch_gemm_any(bf16, kEpiArgmax, a, GemmPlan{kArgmaxWaves, 1}, s);
+    e = launch_gemm_any(bf16, kEpiArgmax, a, lm_head_plan(M), s);
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(argmax_finalize_kernel, dim3(blocks), dim3(threads), 0, s, keys, M, argmax,

@@ -49,6 +49,7 @@ int gemm_k_align(bool bf16);                       // K must be a multiple of th
 // 4, 6 or 8) and the number of K splits.
 struct GemmPlan {
   int nw, splits;
+  int tn = 1;   // 32-column blocks per wave (2 for compute-bound shapes)
 };
 GemmPlan gemm_plan(bool bf16, int M, int N, int K);
 // Plan of two problems of the same K launched together (M2 = 0: one problem).
@@ -66,6 +67,8 @@ hipError_t launch_gemm_partial2(const void* A, int64_t lda, const void* B, int M
 hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t M, int d, int V,
                           unsigned long long* keys, int32_t* argmax, float* max_logit,
                           float* logits, hipStream_t s);
+// Tile shape of the LM head's bf16 kernel for M rows (waves, blocks per wave).
+GemmPlan lm_head_plan(int64_t M);
 
 // ---------------------------------------------------------------- row-wise (rowwise.hip)
 struct QkvEpiArgs {
