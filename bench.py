@@ -41,38 +41,110 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-reducer-stress", action="store_true")
+    ap.add_argument("--no-m-sweep", action="store_true")
+    ap.add_argument("--ragged", action="store_true",
+                    help="also time the 64-sequence ragged decode workload")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 2 GiB device copy (counter calibration)")
     return ap.parse_args()
 
 
-def build_workload(torch, synth, hdf):
+def build_workload(torch, synth, hdf, wl=None):
+    """Device inputs of one warm step of workload wl (default: the full-size step): drafter
+    weights, a KV cache holding every sequence's earlier context rows, the reducer inputs
+    of the newest rows, block tokens and the step's buffers."""
     from paper_2606_26744_amd.step import StepBuffers
-    wl = synth.drafter_full()
+    wl = wl or synth.drafter_full()
     dr = wl.drafter
-    n_seq, T, B, n_s = wl.n_seq, wl.ctx_lens[0], wl.block, wl.new_rows
+    n_seq, B, n_s = wl.n_seq, wl.block, wl.new_rows
+    lens = [int(t) for t in wl.ctx_lens]
+    T = max(lens)
     dev = "cuda"
     w = synth.drafter_weights(wl, device=dev)
     h = hdf.DrafterHandle(w, n_layers=dr.n_layers, d=dr.d, n_heads=dr.n_heads,
                           head_dim=dr.head_dim, d_ff=dr.d_ff, vocab=dr.vocab, eps=dr.eps,
                           rope_theta=dr.rope_theta, rope_max_pos=T + B)
-    offs = hdf.kv_slot_offsets([T] * n_seq)
+    offs = hdf.kv_slot_offsets(lens)
     kv_k, kv_vt = h.alloc_kv(offs[-1])
-    nh, hd = dr.n_heads, dr.head_dim
-    t0 = T - n_s
     for s in range(n_seq):          # rows of earlier rounds, already in the cache
         for l in range(dr.n_layers):
-            k, v = synth.kv_prefix(wl, t0, l, device=dev, sub=s)
+            k, v = synth.kv_prefix(wl, lens[s] - n_s, l, device=dev, sub=s)
             hdf.write_kv_rows(kv_k, kv_vt, l, offs[s], k, v)
+            del k, v
     red = synth.reducer_inputs(wl, n_seq * n_s, device=dev)
     i32 = dict(dtype=torch.int32, device=dev)
     args = dict(H_new=red["H"], W_g=red["W_g"], b_g=red["b_g"],
                 new_offsets=torch.arange(0, n_seq * n_s + 1, n_s, **i32),
-                ctx_len=torch.full((n_seq,), T, **i32), max_ctx=T,
+                ctx_len=torch.tensor(lens, **i32), max_ctx=T,
                 kv_offsets=torch.tensor(offs, **i32), kv_k=kv_k, kv_vt=kv_vt,
                 tokens=synth.block_tokens(wl, device=dev))
     bufs = StepBuffers(h, n_seq, B, n_seq * n_s, T, wl.m)
     return wl, h, bufs, args, red, w, offs
+
+
+def step_targets(torch, synth, hdf, wl, h, bufs, args):
+    """Targets for greedy acceptance: copies of one untimed step's drafts with the
+    workload's per-sequence probability, so acceptance lengths are geometric."""
+    from paper_2606_26744_amd.step import drafter_step
+    out = drafter_step(h, bufs, targets=None, **args)
+    torch.cuda.synchronize()
+    drafts = out["argmax"].view(wl.n_seq, wl.block)[:, 1:].cpu().numpy()
+    return torch.as_tensor(synth.make_targets(drafts, wl.match_p, wl.drafter.vocab,
+                                              seed=wl.seed)).cuda()
+
+
+def ragged_leg(torch, synth, hdf, steps, warmup):
+    """The batched ragged decode workload (64 sequences, contexts U[1024, 16384]):
+    warm-step blocks/s, timed like the headline step."""
+    from paper_2606_26744_amd.step import drafter_step
+    wl, h, bufs, args, red, w, offs = build_workload(torch, synth, hdf, synth.ragged_decode())
+    tg = step_targets(torch, synth, hdf, wl, h, bufs, args)
+    for _ in range(warmup):
+        drafter_step(h, bufs, targets=tg, **args)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        out = drafter_step(h, bufs, targets=tg, **args)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    acc = out["accept_len"].float()
+    res = {"n_seq": wl.n_seq, "context_total": int(sum(wl.ctx_lens)),
+           "context_min": int(min(wl.ctx_lens)), "context_max": int(max(wl.ctx_lens)),
+           "blocks_per_s": round(wl.n_seq / (ms * 1e-3), 1), "ms_per_step": round(ms, 4),
+           "steps": steps, "mean_accept_len": round(float(acc.mean()), 3)}
+    del wl, h, bufs, args, red, w
+    torch.cuda.empty_cache()
+    return res
+
+
+def lm_head_m_sweep(torch, synth, hdf, h, d):
+    """hdf_lm_head_argmax over the full vocabulary at M = 64 .. 2048 rows: time and the
+    fraction of the bf16 matrix-core peak (the knee between the weight stream and the
+    matrix cores)."""
+    out = []
+    for M in (64, 128, 192, 256, 384, 512, 1024, 2048):
+        hid = synth.normal([M, d], 1.0, 7, 50, M, dtype="bf16", device="cuda")
+        ws = torch.zeros(hdf.lm_head_workspace(M, h.V), dtype=torch.uint8, device="cuda")
+        am = torch.empty(M, dtype=torch.int32, device="cuda")
+        for _ in range(2):
+            hdf.lm_head_argmax(hid, h.w_lm, ws=ws, out=(am, None), want_max=False)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        n = 10
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(n):
+            hdf.lm_head_argmax(hid, h.w_lm, ws=ws, out=(am, None), want_max=False)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / n * 1e3
+        tf = 2.0 * M * d * h.V / (us * 1e-6) / 1e12
+        gbs = (h.V * d * 2 + M * d * 2) / (us * 1e-6) / 1e9
+        out.append({"M": M, "us": round(us, 1), "TFLOP/s": round(tf, 1),
+                    "mfma_frac": round(tf / BF16_PEAK_TFLOPS, 4), "GB/s": round(gbs, 1)})
+        del hid, ws, am
+    return out
 
 
 def _kernel_source_sha():
@@ -161,11 +233,7 @@ def main():
     n_seq, B = wl.n_seq, wl.block
     # Targets: copies of the drafts with probability 0.8 per position (drafts from one
     # untimed step), so acceptance lengths are geometric as in the workload description.
-    out = drafter_step(h, bufs, targets=None, **args)
-    torch.cuda.synchronize()
-    drafts = out["argmax"].view(n_seq, B)[:, 1:].cpu().numpy()
-    tg = torch.as_tensor(synth.make_targets(drafts, wl.match_p, wl.drafter.vocab,
-                                            seed=wl.seed)).cuda()
+    tg = step_targets(torch, synth, hdf, wl, h, bufs, args)
     for _ in range(a.warmup):
         drafter_step(h, bufs, targets=tg, **args)
     torch.cuda.synchronize()
@@ -217,6 +285,8 @@ def main():
                      "mfma_frac": round(lm_tflops / BF16_PEAK_TFLOPS, 4)},
         "mean_accept_len": float(acc.mean()), "tau": float(acc.mean() + 1),
     }
+    if not a.no_m_sweep:
+        res["lm_head_m_sweep"] = lm_head_m_sweep(torch, synth, hdf, h, d)
     if not a.no_reducer_stress:
         sw = synth.reducer_stress()
         ri = synth.reducer_inputs(sw, sw.n_tok, device="cuda")
@@ -248,6 +318,10 @@ def main():
         del x, y
     if not a.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(torch, synth, wl, h, w, red, args, offs)
+    if a.ragged:
+        del bufs, args
+        torch.cuda.empty_cache()
+        res["ragged_decode"] = ragged_leg(torch, synth, hdf, max(a.steps // 5, 5), 3)
     print(json.dumps(res), flush=True)
 
 
