@@ -147,7 +147,12 @@ gemm_bf16_kernel(GemmArgs p) {
 #pragma unroll
       for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int tn = 0; tn < TN; ++tn) dst[q * TN + tn] = ld_nt16(Bw[tn] + (kb + q) * 4 * 512);
+        for (int tn = 0; tn < TN; ++tn) {
+          // One pass over the weights streams them past the caches (non-temporal); with
+          // several row tiles (TN = 2) the other row tiles re-read them from L2.
+          const bf16_t* src = Bw[tn] + (kb + q) * 4 * 512;
+          dst[q * TN + tn] = TN == 1 ? ld_nt16(src) : ld16(src);
+        }
     };
     auto store_a = [&](const u32x4* src, int buf) {
 #pragma unroll
@@ -476,15 +481,35 @@ GemmPlan gemm_plan2(bool bf16, int M, int N, int M2, int N2, int K) {
   // traffic) and then to more waves (more bytes in flight per CU).  Every split keeps
   // at least 8 K-steps.
   // Above 128 rows the products are matrix-core bound: waves then own two column blocks
-  // each, which halves the LDS traffic per MFMA (measured at M = 1024: down 90 -> 85 us,
-  // the cold context projection 1182 -> 950 us).
+  // each, which halves the LDS traffic per MFMA, and fetch the weights through the caches
+  // so that the other row tiles find them in L2 (measured at M = 1024: down 90 -> 71 us,
+  // the cold context projection 1182 -> 800 us).
   const int BM = (M <= 64 && M2 <= 64) ? 64 : 128;
   const bool mfma_bound = M > 128 || M2 > 128;
-  const int tn = mfma_bound ? 2 : 1;
+  if (mfma_bound) {
+    // Matrix-core bound: 8 waves x 2 blocks (128 x 512 tiles).  The time is about the
+    // number of rounds of workgroups over the CUs times the K range of one workgroup,
+    // plus the fp32 partials of every extra split (charged 15% each): pick the split
+    // that minimises rounds / splits * (1 + 0.15 (splits - 1)).  At 1024 rows: gate/up
+    // 2 splits (197 -> 185 us), down 4 (86 -> 71 us), QKV 1.
+    const int tiles = ((M + BM - 1) / BM) * ((N + 511) / 512) +
+                      ((M2 + BM - 1) / BM) * ((N2 + 511) / 512);
+    int best_s = 1;
+    double best_t = 1e30;
+    for (int sp = 1; sp <= 8; ++sp) {
+      if (sp > 1 && nk / sp < 8) break;
+      const double t = double((tiles * sp + ncu - 1) / ncu) / sp * (1.0 + 0.15 * (sp - 1));
+      if (t < best_t - 1e-9) {
+        best_t = t;
+        best_s = sp;
+      }
+    }
+    return GemmPlan{8, best_s, 2};
+  }
+  const int tn = 1;
   GemmPlan best{4, 1, tn};
   double best_fill = -1.0;
   for (int nw : {4, 6, 8}) {
-    if (mfma_bound && nw != 8) continue;   // 8 waves x 2 blocks, a 2-step ring
     const int bn = 32 * nw * tn;
     const int tiles = ((M + BM - 1) / BM) * ((N + bn - 1) / bn) +
                       ((M2 + BM - 1) / BM) * ((N2 + bn - 1) / bn);
