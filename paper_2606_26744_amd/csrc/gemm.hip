@@ -57,7 +57,10 @@ __device__ __forceinline__ unsigned long long argmax_key(float v, int col) {
 // LDS feeds TN matrix-core operations, so TN = 2 halves the LDS traffic per MFMA; the
 // compute-bound shapes (a few hundred rows and more) need it, the weight streams of
 // 128 rows prefer more waves per CU instead.
-template <int BM, int NW, int STAGES, int EPI, int TN = 1>
+// NT: fetch the weights with non-temporal loads (they stream past the caches).  Right
+// when one row tile reads every weight byte once; with several row tiles the others
+// re-read the weights from L2, so they are fetched through the caches.
+template <int BM, int NW, int STAGES, int EPI, int TN = 1, bool NT = (TN == 1)>
 __global__ void __launch_bounds__(NW * 64)
 gemm_bf16_kernel(GemmArgs p) {
   constexpr int THREADS = NW * 64;
@@ -148,10 +151,8 @@ gemm_bf16_kernel(GemmArgs p) {
       for (int q = 0; q < 4; ++q)
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) {
-          // One pass over the weights streams them past the caches (non-temporal); with
-          // several row tiles (TN = 2) the other row tiles re-read them from L2.
           const bf16_t* src = Bw[tn] + (kb + q) * 4 * 512;
-          dst[q * TN + tn] = TN == 1 ? ld_nt16(src) : ld16(src);
+          dst[q * TN + tn] = NT ? ld_nt16(src) : ld16(src);
         }
     };
     auto store_a = [&](const u32x4* src, int buf) {
@@ -420,12 +421,19 @@ template <int NW, int TN, int STAGES>
 static void launch_bf16_argmax(const GemmArgs& a, hipStream_t s) {
   const int BM = a.M <= 64 ? 64 : 128;
   constexpr int BN = 32 * NW * TN;
-  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  const int mt = (a.M + BM - 1) / BM;
+  const int tiles = mt * ((a.N + BN - 1) / BN);
   const dim3 grid(tiles, 1, 1), block(NW * 64);
+  // One row tile: every weight byte is read once, so the weights stream past the caches.
   if (BM == 64)
-    hipLaunchKernelGGL((gemm_bf16_kernel<64, NW, STAGES, kEpiArgmax, TN>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<64, NW, STAGES, kEpiArgmax, TN, true>), grid, block, 0,
+                       s, a);
+  else if (mt == 1)
+    hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, STAGES, kEpiArgmax, TN, true>), grid, block, 0,
+                       s, a);
   else
-    hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, STAGES, kEpiArgmax, TN>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, STAGES, kEpiArgmax, TN, (TN == 1)>), grid,
+                       block, 0, s, a);
 }
 
 static hipError_t launch_gemm_any(bool bf16, int epi, const GemmArgs& a, GemmPlan plan,
@@ -442,11 +450,7 @@ static hipError_t launch_gemm_any(bool bf16, int epi, const GemmArgs& a, GemmPla
         launch_bf16_partial<4, 1>(a, plan.splits, s);
       }
     } else {
-      if (plan.tn == 2) {
-        launch_bf16_argmax<8, 2, 2>(a, s);
-      } else {
-        launch_bf16_argmax<8, 1, 2>(a, s);
-      }
+      launch_bf16_argmax<8, 2, 2>(a, s);
     }
     return hipGetLastError();
   }
@@ -565,11 +569,12 @@ hipError_t launch_gemm_partial2(const void* A, int64_t lda, const void* B, int M
   return launch_gemm_any(true, kEpiPartial, a, plan, s);
 }
 
-GemmPlan lm_head_plan(int64_t M) {
-  // 128 rows and fewer: a weight stream, 8 waves of one block each (bytes in flight);
-  // more rows: matrix-core bound, 8 waves of two blocks each (half the LDS traffic per
-  // MFMA; M = 1024: 914 -> 848 us).
-  return M <= 128 ? GemmPlan{8, 1, 1} : GemmPlan{8, 1, 2};
+GemmPlan lm_head_plan(int64_t) {
+  // 8 waves of two 32-column blocks each (512-column tiles).  Above 128 rows the product
+  // is matrix-core bound and two blocks per wave halve the LDS traffic per MFMA (M = 1024:
+  // 914 -> 848 us); at 128 rows and fewer it is a weight stream, and the wider tile halves
+  // the activation bytes each CU reads per weight byte (M = 128: 173 -> 166 us).
+  return GemmPlan{8, 1, 2};
 }
 
 hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t M, int d, int V,
