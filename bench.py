@@ -44,6 +44,11 @@ def parse():
     ap.add_argument("--no-m-sweep", action="store_true")
     ap.add_argument("--ragged", action="store_true",
                     help="also time the 64-sequence ragged decode workload")
+    ap.add_argument("--cold", action="store_true",
+                    help="also time the cold step (every context row reduced and projected)")
+    ap.add_argument("--blas-ref", action="store_true",
+                    help="also time the vendor BLAS (torch.matmul) on the matrix-core bound "
+                         "GEMM shapes, for context")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 2 GiB device copy (counter calibration)")
     return ap.parse_args()
@@ -93,11 +98,12 @@ def step_targets(torch, synth, hdf, wl, h, bufs, args):
                                               seed=wl.seed)).cuda()
 
 
-def ragged_leg(torch, synth, hdf, steps, warmup):
-    """The batched ragged decode workload (64 sequences, contexts U[1024, 16384]):
-    warm-step blocks/s, timed like the headline step."""
+def ragged_leg(torch, synth, hdf, steps, warmup, wl=None):
+    """A further step workload, timed like the headline step: by default the batched ragged
+    decode workload (64 sequences, contexts U[1024, 16384]), warm-step blocks/s."""
     from paper_2606_26744_amd.step import drafter_step
-    wl, h, bufs, args, red, w, offs = build_workload(torch, synth, hdf, synth.ragged_decode())
+    wl, h, bufs, args, red, w, offs = build_workload(torch, synth, hdf,
+                                                     wl or synth.ragged_decode())
     tg = step_targets(torch, synth, hdf, wl, h, bufs, args)
     for _ in range(warmup):
         drafter_step(h, bufs, targets=tg, **args)
@@ -144,6 +150,38 @@ def lm_head_m_sweep(torch, synth, hdf, h, d):
         out.append({"M": M, "us": round(us, 1), "TFLOP/s": round(tf, 1),
                     "mfma_frac": round(tf / BF16_PEAK_TFLOPS, 4), "GB/s": round(gbs, 1)})
         del hid, ws, am
+    return out
+
+
+def blas_reference(torch):
+    """torch.matmul (the vendor BLAS) on the matrix-core bound GEMM shapes of the drafter,
+    with the bench's value distributions (activations N(0, 1), weights N(0, 0.02), bf16):
+    what the library reaches on the same shapes and data, beside this path's own kernels."""
+    shapes = [("lm_head", 1024, 4096, 129280), ("gate_up", 1024, 4096, 24576),
+              ("down", 1024, 12288, 4096), ("qkv", 1024, 4096, 12288),
+              ("ctx_kv_cold", 16384, 4096, 8192)]
+    g = torch.Generator(device="cuda").manual_seed(7)
+    out = []
+    for name, M, K, N in shapes:
+        a = torch.randn((M, K), generator=g, device="cuda").to(torch.bfloat16)
+        w = (torch.randn((N, K), generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+        wt = w.t()
+        for _ in range(3):
+            c = torch.matmul(a, wt)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        n = 10
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(n):
+            c = torch.matmul(a, wt)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / n * 1e3
+        tf = 2.0 * M * N * K / (us * 1e-6) / 1e12
+        out.append({"gemm": name, "M": M, "K": K, "N": N, "us": round(us, 1),
+                    "TFLOP/s": round(tf, 1), "mfma_frac": round(tf / BF16_PEAK_TFLOPS, 4)})
+        del a, w, wt, c
+        torch.cuda.empty_cache()
     return out
 
 
@@ -318,10 +356,16 @@ def main():
         del x, y
     if not a.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(torch, synth, wl, h, w, red, args, offs)
-    if a.ragged:
+    if a.blas_ref:
+        res["blas_reference"] = blas_reference(torch)
+    if a.ragged or a.cold:
         del bufs, args
         torch.cuda.empty_cache()
+    if a.ragged:
         res["ragged_decode"] = ragged_leg(torch, synth, hdf, max(a.steps // 5, 5), 3)
+    if a.cold:
+        res["drafter_full_cold"] = ragged_leg(torch, synth, hdf, max(a.steps // 5, 5), 3,
+                                              synth.drafter_full_cold())
     print(json.dumps(res), flush=True)
 
 

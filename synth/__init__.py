@@ -142,6 +142,15 @@ def drafter_full() -> Workload:
                     match_p=[0.8] * 8, new_rows=16)
 
 
+def drafter_full_cold() -> Workload:
+    """Cold step of the full-size drafter: the cache starts empty and every one of the
+    2048 context rows of each of the 8 sequences is reduced and projected in the step."""
+    wl = drafter_full()
+    wl.name = "drafter_full_cold"
+    wl.new_rows = 2048
+    return wl
+
+
 def ragged_decode(n_seq: int = 64) -> Workload:
     """Batched ragged decode: 64 sequences, context lengths U[1024, 16384], same drafter
     as the full-size step, per-sequence copy probability U[0.3, 0.95]."""
@@ -160,6 +169,7 @@ WORKLOADS = {
     "small_bf16": small_bf16,
     "reducer_stress": reducer_stress,
     "drafter_full": drafter_full,
+    "drafter_full_cold": drafter_full_cold,
     "ragged_decode": ragged_decode,
 }
 

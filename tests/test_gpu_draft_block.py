@@ -99,6 +99,17 @@ def test_full_size_warm_sampled():
     torch.cuda.empty_cache()
 
 
+def test_full_size_cold_sampled():
+    """Full-size cold step: every one of the 8 x 2048 context rows is projected in the call
+    (a 16384-row context projection on the matrix cores, grouped with the block's QKV);
+    the oracle evaluates one sequence and all 2048 of its cache rows."""
+    wl = synth.drafter_full()
+    case = DraftCase(wl, [2048] * 8, [2048] * 8, random_norms=False, sub=8)
+    _compare(case, seqs=[6])
+    del case
+    torch.cuda.empty_cache()
+
+
 def test_ragged_long_contexts_sampled():
     wl = synth.ragged_decode()
     ctx = [1024, 16384, 5000, 777 + 1024]
