@@ -1,53 +1,91 @@
 // Greedy acceptance (Sec. 1: the target keeps the longest agreeing draft prefix;
 // Sec. 3.4: tau, the accepted length per round).
 //
-// One workgroup: each thread scans one sequence's drafts for the first mismatch,
-// then a workgroup prefix sum over (n_s + 1) gives the packed commit offsets, and
-// each thread copies its committed target tokens.  Sequences beyond the
-// workgroup size are handled in successive passes with a running carry.
+// One workgroup of 16 waves, sequences in chunks of 1024:
+//   1. one wave per sequence: its lanes compare 64 draft positions at once (ballot of
+//      the mismatches, with a sentinel at position K), so n_s costs one round of loads;
+//   2. an exclusive prefix sum over the chunk's (n_s + 1) (wave scans, then the wave
+//      totals) gives the packed commit offsets, continued across chunks by a carry;
+//   3. one wave per sequence copies its n_s + 1 committed target tokens.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace hdf {
 
 constexpr int kAcceptThreads = 1024;
+constexpr int kAcceptWaves = kAcceptThreads / kWave;
 
 __global__ void __launch_bounds__(kAcceptThreads)
 accept_kernel(const int32_t* __restrict__ draft, int stride, const int32_t* __restrict__ target,
               int n_seq, int K, int32_t* __restrict__ acc, int32_t* __restrict__ anchor,
               int32_t* __restrict__ offs, int32_t* __restrict__ toks) {
-  __shared__ int scan[kAcceptThreads];
+  __shared__ int len[kAcceptThreads];     // n_s + 1, then the exclusive offsets
+  __shared__ int nacc[kAcceptThreads];    // n_s
+  __shared__ int wsum[kAcceptWaves];
   const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wid = tid >> 6;
   int carry = 0;
   for (int base = 0; base < n_seq; base += kAcceptThreads) {
-    const int s = base + tid;
-    int n = 0;
-    if (s < n_seq) {
-      const int32_t* dr = draft + int64_t(s) * stride;
-      const int32_t* tg = target + int64_t(s) * (K + 1);
-      while (n < K && dr[n] == tg[n]) ++n;
-      acc[s] = n;
-      anchor[s] = tg[n];
-    }
-    const int v = (s < n_seq) ? n + 1 : 0;
-    scan[tid] = v;
-    __syncthreads();
-    // Hillis-Steele inclusive scan.
-    for (int o = 1; o < kAcceptThreads; o <<= 1) {
-      const int add = (tid >= o) ? scan[tid - o] : 0;
-      __syncthreads();
-      scan[tid] += add;
-      __syncthreads();
-    }
-    const int excl = carry + scan[tid] - v;
-    if (s < n_seq) {
-      if (offs != nullptr) offs[s] = excl;
-      if (toks != nullptr) {
-        const int32_t* tg = target + int64_t(s) * (K + 1);
-        for (int i = 0; i <= n; ++i) toks[excl + i] = tg[i];
+    const int cnt = min(kAcceptThreads, n_seq - base);
+    for (int j = wid; j < cnt; j += kAcceptWaves) {
+      const int64_t s = base + j;
+      const int32_t* dr = draft + s * stride;
+      const int32_t* tg = target + s * (K + 1);
+      int n = K, an = 0;
+      for (int c0 = 0; c0 <= K; c0 += kWave) {
+        const int i = c0 + lane;
+        const int32_t dv = i < K ? dr[i] : 0;
+        const int32_t tv = i <= K ? tg[i] : 0;
+        unsigned long long miss = __ballot(i < K && dv != tv);
+        if (K - c0 < kWave) miss |= 1ull << (K - c0);    // position K ends every scan
+        if (miss != 0ull) {
+          const int f = __ffsll(static_cast<long long>(miss)) - 1;
+          n = c0 + f;
+          an = __shfl(tv, f, kWave);
+          break;
+        }
+      }
+      if (lane == 0) {
+        acc[s] = n;
+        anchor[s] = an;
+        len[j] = n + 1;
+        nacc[j] = n;
       }
     }
-    carry += scan[kAcceptThreads - 1];
+    __syncthreads();
+    // Exclusive scan of len[0 .. cnt): inclusive scan inside each wave, then the totals.
+    int v = tid < cnt ? len[tid] : 0;
+    int incl = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int t = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += t;
+    }
+    if (lane == kWave - 1) wsum[wid] = incl;
+    __syncthreads();
+    int before = 0, total = 0;
+    for (int w = 0; w < kAcceptWaves; ++w) {
+      const int ws = wsum[w];
+      if (w < wid) before += ws;
+      total += ws;
+    }
+    const int excl = carry + before + incl - v;
+    if (tid < cnt) {
+      len[tid] = excl;
+      if (offs != nullptr) offs[base + tid] = excl;
+    }
+    __syncthreads();
+    if (toks != nullptr) {
+      for (int j = wid; j < cnt; j += kAcceptWaves) {
+        const int64_t s = base + j;
+        const int n = nacc[j];
+        const int o = len[j];
+        const int32_t* tg = target + s * (K + 1);
+        for (int i = lane; i <= n; i += kWave) toks[o + i] = tg[i];
+      }
+    }
+    carry += total;
     __syncthreads();
   }
   if (offs != nullptr && tid == 0) offs[n_seq] = carry;

@@ -44,7 +44,9 @@ def test_k_zero():
     assert acc.tolist() == [0, 0, 0] and anc.tolist() == [4, 5, 6] and offs.tolist() == [0, 1, 2, 3]
 
 
-@pytest.mark.parametrize("n_seq,K,p", [(8, 15, 0.8), (64, 15, 0.5), (3000, 15, 0.9), (5, 200, 0.99)])
+@pytest.mark.parametrize("n_seq,K,p", [(8, 15, 0.8), (64, 15, 0.5), (3000, 15, 0.9), (5, 200, 0.99),
+                                        (4, 63, 1.0), (4, 64, 1.0), (3, 128, 1.0), (2, 1024, 1.0),
+                                        (1025, 64, 0.95)])
 def test_random_geometric(n_seq, K, p):
     rng = np.random.default_rng(n_seq + K)
     drafts = rng.integers(0, 129280, (n_seq, K))
