@@ -64,6 +64,13 @@ constexpr int64_t kCtxChunk = 16384;  // context rows projected per GEMM launch
 // (8 x 2048 cold rows: 9 rounds of workgroups instead of 8, 1032 -> 927 us).
 constexpr int64_t kGroupRows = 2048;
 
+// Up to 128 context rows and 128 block rows: one problem takes both row sets over the
+// K/V columns (two row tiles streaming the same weights through L2), the other the block
+// rows over the Q columns, so the K/V weights are fetched once per layer, not twice.
+bool kv_shared(bool bf, int64_t n_new, size_t M) {
+  return bf && n_new > 0 && n_new <= 128 && M <= 128;
+}
+
 hdf_status validate_drafter(const hdf_drafter* w) {
   if (w == nullptr) return fail(HDF_E_INVALID, "drafter: null");
   if (w->dtype != HDF_F32 && w->dtype != HDF_BF16) return fail(HDF_E_INVALID, "drafter: bad dtype");
@@ -126,7 +133,13 @@ DraftPlan plan_workspace(const hdf_drafter& w, int n_seq, int B, int64_t n_new, 
   };
   upd(crow, 2 * w.d, w.d);
   upd(n_new % kCtxChunk, 2 * w.d, w.d);  // a shorter last chunk may split further
-  if (bf && n_new > 0 && n_new <= kGroupRows) {
+  if (kv_shared(bf, n_new, M)) {
+    // [context rows; block rows] x K/V and block rows x Q in one launch.
+    const int rows1 = int(n_new + M);
+    const size_t sp = size_t(hdf::gemm_plan_shared(rows1, 2 * w.d, int(M), w.d, w.d).splits);
+    const size_t b = sp * (size_t(rows1) * 2 * w.d + M * w.d) * 4;
+    if (b > parts) parts = b;
+  } else if (bf && n_new > 0 && n_new <= kGroupRows) {
     // Context K/V and block QKV in one launch: both problems' partials.
     const size_t sp = size_t(hdf::gemm_plan2(bf, int(n_new), 2 * w.d, int(M), 3 * w.d, w.d).splits);
     const size_t b = sp * (size_t(n_new) * 2 * w.d + M * 3 * w.d) * 4;
@@ -144,9 +157,11 @@ DraftPlan plan_workspace(const hdf_drafter& w, int n_seq, int B, int64_t n_new, 
   };
   P.plan_pos = take(size_t(n_new) * 4);
   P.plan_row = take(size_t(n_new) * 4);
-  P.c = take(size_t(crow) * d * el);
+  // The block rows' normed states u follow the context rows' c, so that one GEMM
+  // problem can take both row sets.
+  P.c = take((size_t(crow) + M) * d * el);
+  P.u = P.c + size_t(crow) * d * el;
   P.h = take(M * d * 4);
-  P.u = take(M * d * el);
   P.q = take(M * d * el);
   P.kb = take(size_t(w.n_heads) * size_t(n_seq) * 64 * w.head_dim * el);
   P.vtb = take(size_t(w.n_heads) * size_t(n_seq) * 64 * w.head_dim * el);
@@ -322,7 +337,8 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
   };
   auto ctx_epi = [&](int l, int64_t r0, int rows, int S, const float* pp) {
     hdf::QkvEpiArgs ea{};
-    ea.parts = pp; ea.S = S; ea.M = rows; ea.first_part = 1;
+    ea.pkv = pp; ea.ld_kv = 2 * int64_t(d); ea.zs_kv = int64_t(rows) * 2 * d;
+    ea.S = S; ea.M = rows; ea.first_part = 1;
     ea.d = d; ea.nh = nh; ea.hd = hd; ea.B = B;
     ea.ctx_len = ctx_len; ea.plan_pos = plan_pos + r0; ea.plan_row = plan_row + r0;
     ea.rope_cs = w->rope_cs;
@@ -334,7 +350,9 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
   };
   auto blk_epi = [&](int S, const float* pp) {
     hdf::QkvEpiArgs ea{};
-    ea.parts = pp; ea.S = S; ea.M = M; ea.first_part = 0;
+    ea.pq = pp; ea.ld_q = 3 * int64_t(d); ea.zs_q = int64_t(M) * 3 * d;
+    ea.pkv = pp + d; ea.ld_kv = ea.ld_q; ea.zs_kv = ea.zs_q;
+    ea.S = S; ea.M = M; ea.first_part = 0;
     ea.d = d; ea.nh = nh; ea.hd = hd; ea.B = B;
     ea.ctx_len = ctx_len; ea.rope_cs = w->rope_cs;
     ea.q = q; ea.k = kb; ea.vt = vtb; ea.cap = capb;
@@ -345,6 +363,7 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
   // the block's Q/K/V (below); otherwise K/V of every layer go into the cache here, in
   // chunks of kCtxChunk rows.
   const bool grouped = bf && n_new > 0 && n_new <= kGroupRows;
+  const bool shared = kv_shared(bf, n_new, size_t(M));
   if (n_new == 0) HDF_TRY(prep(0, 0, true));
   if (grouped) HDF_TRY(prep(0, int(n_new), true));
   for (int64_t r0 = 0; !grouped && r0 < n_new; r0 += kCtxChunk) {
@@ -362,7 +381,22 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
   const int n_chunks = (max_ctx + P.chunk_len - 1) / P.chunk_len;
   for (int l = 0; l < L; ++l) {
     // Q, K_b, V_b with RoPE at T_s + k (and the context rows' K/V when grouped).
-    if (grouped) {
+    if (shared) {
+      const char* wkv = static_cast<const char*>(w->w_qkv[l]) + size_t(d) * d * el;
+      const int rows1 = int(n_new) + M;
+      const hdf::GemmPlan Sg = hdf::gemm_plan_shared(rows1, 2 * d, M, d, d);
+      float* parts_kv = parts;                                       // [S][rows1][2d]
+      float* parts_q = parts + size_t(Sg.splits) * rows1 * 2 * d;    // [S][M][d]
+      HDF_TRY(hdf::launch_gemm_partial2(cbuf, d, wkv, rows1, 2 * d, parts_kv, u, d, w->w_qkv[l],
+                                        M, d, parts_q, d, Sg, s));
+      hdf::QkvEpiArgs ce = ctx_epi(l, 0, int(n_new), Sg.splits, parts_kv);
+      ce.zs_kv = int64_t(rows1) * 2 * d;
+      hdf::QkvEpiArgs be = blk_epi(Sg.splits, parts_q);
+      be.pq = parts_q; be.ld_q = d; be.zs_q = int64_t(M) * d;
+      be.pkv = parts_kv + size_t(n_new) * 2 * d; be.ld_kv = 2 * int64_t(d);
+      be.zs_kv = ce.zs_kv;
+      HDF_TRY(hdf::launch_qkv_epilogue2(bf, ce, be, s));
+    } else if (grouped) {
       const char* wkv = static_cast<const char*>(w->w_qkv[l]) + size_t(d) * d * el;
       const int rows = int(n_new);
       const hdf::GemmPlan Sg = hdf::gemm_plan2(bf, rows, 2 * d, M, 3 * d, d);

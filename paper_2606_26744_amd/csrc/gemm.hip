@@ -26,6 +26,8 @@
 //
 // fp32 (small correctness-size workloads): a plain LDS-tiled VALU kernel reading the
 // same packed weight layout, with the same epilogues.
+#include <initializer_list>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -404,7 +406,7 @@ __global__ void pack_weight_kernel(const T* __restrict__ src, T* __restrict__ ds
 
 // ---------------------------------------------------------------------------- host side
 
-template <int NW, int TN, int STAGES = 4>
+template <int NW, int TN, int STAGES = 4, bool NT = (TN == 1)>
 static void launch_bf16_partial(const GemmArgs& a, int splits, hipStream_t s) {
   const int BM = (a.M <= 64 && a.M2 <= 64) ? 64 : 128;
   constexpr int BN = 32 * NW * TN;
@@ -412,9 +414,11 @@ static void launch_bf16_partial(const GemmArgs& a, int splits, hipStream_t s) {
                     ((a.M2 + BM - 1) / BM) * ((a.N2 + BN - 1) / BN);
   const dim3 grid(tiles, 1, splits), block(NW * 64);
   if (BM == 64)
-    hipLaunchKernelGGL((gemm_bf16_kernel<64, NW, STAGES, kEpiPartial, TN>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<64, NW, STAGES, kEpiPartial, TN, NT>), grid, block, 0, s,
+                       a);
   else
-    hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, STAGES, kEpiPartial, TN>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, STAGES, kEpiPartial, TN, NT>), grid, block, 0,
+                       s, a);
 }
 
 template <int NW, int TN, int STAGES>
@@ -442,6 +446,8 @@ static hipError_t launch_gemm_any(bool bf16, int epi, const GemmArgs& a, GemmPla
     if (epi == kEpiPartial) {
       if (plan.tn == 2) {
         launch_bf16_partial<8, 2, 2>(a, plan.splits, s);
+      } else if (!plan.nt) {
+        launch_bf16_partial<8, 1, 4, false>(a, plan.splits, s);
       } else if (plan.nw == 8) {
         launch_bf16_partial<8, 1>(a, plan.splits, s);
       } else if (plan.nw == 6) {
@@ -467,6 +473,9 @@ static hipError_t launch_gemm_any(bool bf16, int epi, const GemmArgs& a, GemmPla
 int gemm_k_align(bool bf16) { return bf16 ? kBK : 16; }
 
 GemmPlan gemm_plan(bool bf16, int M, int N, int K) { return gemm_plan2(bf16, M, N, 0, 0, K); }
+
+static GemmPlan plan_stream(int BM, int M, int N, int M2, int N2, int nk, int ncu,
+                            std::initializer_list<int> waves);
 
 GemmPlan gemm_plan2(bool bf16, int M, int N, int M2, int N2, int K) {
   const int ncu = device_cu_count();
@@ -510,10 +519,23 @@ GemmPlan gemm_plan2(bool bf16, int M, int N, int M2, int N2, int K) {
     }
     return GemmPlan{8, best_s, 2};
   }
+  return plan_stream(BM, M, N, M2, N2, nk, ncu, {4, 6, 8});
+}
+
+GemmPlan gemm_plan_shared(int M, int N, int M2, int N2, int K) {
+  // The row tiles of the first problem (at most two) read the same weight columns at
+  // about the same time on one XCD: 8-wave tiles with the weights fetched through L2.
+  GemmPlan p = plan_stream(128, M, N, M2, N2, K / kBK, device_cu_count(), {8});
+  p.nt = false;
+  return p;
+}
+
+static GemmPlan plan_stream(int BM, int M, int N, int M2, int N2, int nk, int ncu,
+                            std::initializer_list<int> waves) {
   const int tn = 1;
   GemmPlan best{4, 1, tn};
   double best_fill = -1.0;
-  for (int nw : {4, 6, 8}) {
+  for (int nw : waves) {
     const int bn = 32 * nw * tn;
     const int tiles = ((M + BM - 1) / BM) * ((N + bn - 1) / bn) +
                       ((M2 + BM - 1) / BM) * ((N2 + bn - 1) / bn);

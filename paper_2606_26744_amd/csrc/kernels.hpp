@@ -49,11 +49,15 @@ int gemm_k_align(bool bf16);                       // K must be a multiple of th
 // 4, 6 or 8) and the number of K splits.
 struct GemmPlan {
   int nw, splits;
-  int tn = 1;   // 32-column blocks per wave (2 for compute-bound shapes)
+  int tn = 1;       // 32-column blocks per wave (2 for compute-bound shapes)
+  bool nt = true;   // one-block waves: weights streamed past the caches
 };
 GemmPlan gemm_plan(bool bf16, int M, int N, int K);
 // Plan of two problems of the same K launched together (M2 = 0: one problem).
 GemmPlan gemm_plan2(bool bf16, int M, int N, int M2, int N2, int K);
+// Two problems of the same K in one launch where the first one's row tiles (up to 256
+// rows) share weight columns: weights fetched through L2 (8 waves of one block).
+GemmPlan gemm_plan_shared(int M, int N, int M2, int N2, int K);
 size_t packed_weight_elems(int N, int K);          // rows rounded up to 128
 hipError_t launch_pack_weight(bool bf16, const void* src, void* dst, int N, int K, hipStream_t s);
 // C[z][M][N] (fp32) = A[M][K] . W[N][K]^T over the z-th of `splits` K ranges; W packed.
@@ -72,9 +76,14 @@ GemmPlan lm_head_plan(int64_t M);
 
 // ---------------------------------------------------------------- row-wise (rowwise.hip)
 struct QkvEpiArgs {
-  const float* parts;    // [S][M][n_parts*d]
+  // Split-K partials of the rows' projections: split z of row r, column j of Q at
+  // pq[z*zs_q + r*ld_q + j], of K at pkv[z*zs_kv + r*ld_kv + j], of V at the same + d.
+  const float* pq;
+  int64_t ld_q, zs_q;
+  const float* pkv;
+  int64_t ld_kv, zs_kv;
   int S, M;
-  int first_part;        // 0: parts are Q,K,V (block rows); 1: parts are K,V (context rows)
+  int first_part;        // 0: Q, K, V (block rows); 1: K, V only (context rows)
   int d, nh, hd, B;
   const int32_t* ctx_len;   // block rows: position = ctx_len[s] + k
   const int32_t* plan_pos;  // context rows: position and cache row per row

@@ -198,8 +198,6 @@ qkv_epilogue_kernel(QkvEpiArgs a0, QkvEpiArgs a1, int nb0) {
   const int r0 = (second ? int(blockIdx.x) - nb0 : int(blockIdx.x)) * kQkvRows;
   const int h = blockIdx.y;
   const int rows = min(kQkvRows, a.M - r0);
-  const int ncol = (3 - a.first_part) * a.d;
-  const int64_t zstride = int64_t(a.M) * ncol;
   if (threadIdx.x < rows) {
     int pos, s, k;
     int64_t drow;
@@ -219,12 +217,15 @@ qkv_epilogue_kernel(QkvEpiArgs a0, QkvEpiArgs a1, int nb0) {
     const int pp = rem / QUADS;
     const int i0 = (rem - pp * QUADS) * 4;
     const int part = a.first_part + pp;
-    const int64_t c = int64_t(r0 + rr) * ncol + int64_t(pp) * a.d + int64_t(h) * HD + i0;
-    float4 x1 = *reinterpret_cast<const float4*>(a.parts + c);
-    float4 x2 = *reinterpret_cast<const float4*>(a.parts + c + HALF);
+    const float* src = part == 0 ? a.pq : a.pkv;
+    const int64_t ld = part == 0 ? a.ld_q : a.ld_kv;
+    const int64_t zstride = part == 0 ? a.zs_q : a.zs_kv;
+    const int64_t c = int64_t(r0 + rr) * ld + int64_t(h) * HD + i0;
+    float4 x1 = *reinterpret_cast<const float4*>(src + c);
+    float4 x2 = *reinterpret_cast<const float4*>(src + c + HALF);
     for (int z = 1; z < a.S; ++z) {
-      const float4 t1 = *reinterpret_cast<const float4*>(a.parts + z * zstride + c);
-      const float4 t2 = *reinterpret_cast<const float4*>(a.parts + z * zstride + c + HALF);
+      const float4 t1 = *reinterpret_cast<const float4*>(src + z * zstride + c);
+      const float4 t2 = *reinterpret_cast<const float4*>(src + z * zstride + c + HALF);
       x1.x += t1.x; x1.y += t1.y; x1.z += t1.z; x1.w += t1.w;
       x2.x += t2.x; x2.y += t2.y; x2.z += t2.z; x2.w += t2.w;
     }
@@ -250,14 +251,14 @@ qkv_epilogue_kernel(QkvEpiArgs a0, QkvEpiArgs a1, int nb0) {
     }
   }
   // V part -> LDS.
-  const int64_t vcol = int64_t(2 - a.first_part) * a.d + int64_t(h) * HD;
+  const float* vsrc = a.pkv + a.d + int64_t(h) * HD;
   for (int e = threadIdx.x; e < rows * (HD / 4); e += kRowThreads) {
     const int rr = e / (HD / 4);
     const int i0 = (e - rr * (HD / 4)) * 4;
-    const int64_t c = int64_t(r0 + rr) * ncol + vcol + i0;
-    float4 x = *reinterpret_cast<const float4*>(a.parts + c);
+    const int64_t c = int64_t(r0 + rr) * a.ld_kv + i0;
+    float4 x = *reinterpret_cast<const float4*>(vsrc + c);
     for (int z = 1; z < a.S; ++z) {
-      const float4 t = *reinterpret_cast<const float4*>(a.parts + z * zstride + c);
+      const float4 t = *reinterpret_cast<const float4*>(vsrc + z * a.zs_kv + c);
       x.x += t.x; x.y += t.y; x.z += t.z; x.w += t.w;
     }
     vt_tile[rr][i0 + 0] = x.x;
