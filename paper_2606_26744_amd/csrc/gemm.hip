@@ -62,7 +62,9 @@ __device__ __forceinline__ unsigned long long argmax_key(float v, int col) {
 // NT: fetch the weights with non-temporal loads (they stream past the caches).  Right
 // when one row tile reads every weight byte once; with several row tiles the others
 // re-read the weights from L2, so they are fetched through the caches.
-template <int BM, int NW, int STAGES, int EPI, int TN = 1, bool NT = (TN == 1)>
+// PP: the ping-pong K loop of the matrix-core bound tiles (128 x 512, 8 waves of two
+// blocks): the two waves of a SIMD alternate between a memory phase and a compute phase.
+template <int BM, int NW, int STAGES, int EPI, int TN = 1, bool NT = (TN == 1), bool PP = false>
 __global__ void __launch_bounds__(NW * 64)
 gemm_bf16_kernel(GemmArgs p) {
   constexpr int THREADS = NW * 64;
@@ -76,7 +78,8 @@ gemm_bf16_kernel(GemmArgs p) {
   static_assert(EPI != kEpiArgmax || NB % 4 == 0, "argmax tiles are whole 128-column slabs");
   // LDS: the double-buffered activation tile, reused after the K loop by the ARGMAX
   // epilogue to stage the fp32 tile of four waves at a time ([wave][row][32 columns]).
-  constexpr size_t kMainLds = size_t(2) * BM * LDA * sizeof(bf16_t);
+  constexpr size_t kMainLds = PP ? size_t(4) * BM * (32 + 8) * sizeof(bf16_t)   // NBUF units
+                                : size_t(2) * BM * LDA * sizeof(bf16_t);
   constexpr size_t kEpiLds = (EPI == kEpiArgmax) ? size_t(4) * BM * LDC * sizeof(float) : 0;
   __shared__ __attribute__((aligned(16))) unsigned char smem[kMainLds > kEpiLds ? kMainLds : kEpiLds];
   typedef bf16_t ATile[BM][LDA];
@@ -132,7 +135,91 @@ gemm_bf16_kernel(GemmArgs p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][tn][r] = 0.f;
 
-  if (nk > 0) {
+  if constexpr (PP) {
+    // Waves 4-7 (group 1) run one phase behind waves 0-3 (group 0); the two waves of a
+    // SIMD come one from each group.  In its memory phase a wave reads the activation
+    // fragments of its next unit (32 of K) from LDS, stores its share of a later unit's
+    // activations into LDS and issues the weight loads of the unit D ahead; in its
+    // compute phase it runs the unit's 16 MFMAs from registers only.  A workgroup
+    // barrier ends every phase, so while one wave of a SIMD computes, the other loads.
+    static_assert(BM == 128 && NW == 8 && TN == 2, "ping-pong tiles are 128 x 512, 8 waves");
+    constexpr int UK = 32;                   // K of one unit (two MFMA sub-steps)
+    constexpr int LDU = UK + 8;              // padded LDS row of a unit (bf16 elements)
+    constexpr int NBUF = 4;                  // LDS buffers of activation units
+    constexpr int D = 2;                     // weight units in flight ahead of their use
+    constexpr int NR = D + 1;
+    static_assert(size_t(NBUF) * BM * LDU * sizeof(bf16_t) <= sizeof(smem), "LDS");
+    typedef bf16_t UTile[BM][LDU];
+    UTile* Au = reinterpret_cast<UTile*>(smem);
+    const int nu = nk * (kBK / UK);
+    const int64_t ku0 = int64_t(kt_begin) * (kBK / UK);
+    const int grp = wid >> 2;
+    // Activation staging: thread tid moves row tid/4, 16-byte chunk tid%4 of each unit
+    // (512 threads x 16 B = one 128 x 32 unit).  Rows past M are clamped, units past the
+    // end re-read the last one; neither is ever used.
+    const bf16_t* a_src = A + int64_t(min(m0 + (tid >> 2), p.M - 1)) * p.lda + (tid & 3) * 8;
+    auto a_load = [&](int u) { return ld16(a_src + (ku0 + min(u, nu - 1)) * UK); };
+    auto a_store = [&](const u32x4& v, int u) {
+      *reinterpret_cast<u32x4*>(&Au[u % NBUF][tid >> 2][(tid & 3) * 8]) = v;
+    };
+    auto b_load = [&](int u, u32x4* dst) {
+      const int64_t kb = (ku0 + min(u, nu - 1)) * (UK / 16);
+#pragma unroll
+      for (int ss = 0; ss < 2; ++ss)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) dst[ss * TN + tn] = ld16(Bw[tn] + (kb + ss) * 4 * 512);
+    };
+    const int arow = lane & 31;
+    const int kof = 8 * (lane >> 5);
+    if (nu > 0) {
+      u32x4 rb[NR][2 * TN];
+      u32x4 areg = a_load(0);
+      a_store(areg, 0);
+      areg = a_load(1);
+      a_store(areg, 1);
+      areg = a_load(2);
+#pragma unroll
+      for (int j = 0; j < D; ++j) b_load(j, rb[j]);
+      __syncthreads();
+      if (grp == 1) __syncthreads();   // group 1 starts one phase behind
+      // Unit u: buffer u % NBUF holds its activations (written during the memory phases
+      // of unit u-2 by both groups); rb[slot] its weights (loaded D units earlier).
+      auto unit = [&](int u, int slot) {
+        bf16x8_t af[2][TM];
+#pragma unroll
+        for (int ss = 0; ss < 2; ++ss)
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+            af[ss][i] = *reinterpret_cast<const bf16x8_t*>(
+                &Au[u % NBUF][arow + 32 * i][ss * 16 + kof]);
+        a_store(areg, u + 2);
+        areg = a_load(u + 3);
+        b_load(u + D, rb[(slot + D) % NR]);
+        __syncthreads();
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int ss = 0; ss < 2; ++ss)
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int tn = 0; tn < TN; ++tn)
+              acc[i][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                  af[ss][i], __builtin_bit_cast(bf16x8_t, rb[slot][ss * TN + tn]), acc[i][tn],
+                  0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+      };
+      int u = 0;
+      for (; u + NR <= nu; u += NR) {
+#pragma unroll
+        for (int j = 0; j < NR; ++j) unit(u + j, j);
+      }
+#pragma unroll
+      for (int j = 0; j < NR; ++j)
+        if (u + j < nu) unit(u + j, j);
+      if (grp == 0) __syncthreads();   // group 0 ends one phase later
+    }
+  } else if (nk > 0) {
     u32x4 ra[STAGES][A_CH];
     u32x4 rb[STAGES][TN * 4];
     // Activation chunk c of a K-step: row c/8, 16-byte column c%8.  Rows past M are
@@ -406,7 +493,7 @@ __global__ void pack_weight_kernel(const T* __restrict__ src, T* __restrict__ ds
 
 // ---------------------------------------------------------------------------- host side
 
-template <int NW, int TN, int STAGES = 4, bool NT = (TN == 1)>
+template <int NW, int TN, int STAGES = 4, bool NT = (TN == 1), bool PP = (TN == 2)>
 static void launch_bf16_partial(const GemmArgs& a, int splits, hipStream_t s) {
   const int BM = (a.M <= 64 && a.M2 <= 64) ? 64 : 128;
   constexpr int BN = 32 * NW * TN;
@@ -417,8 +504,8 @@ static void launch_bf16_partial(const GemmArgs& a, int splits, hipStream_t s) {
     hipLaunchKernelGGL((gemm_bf16_kernel<64, NW, STAGES, kEpiPartial, TN, NT>), grid, block, 0, s,
                        a);
   else
-    hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, STAGES, kEpiPartial, TN, NT>), grid, block, 0,
-                       s, a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, STAGES, kEpiPartial, TN, NT, PP>), grid, block,
+                       0, s, a);
 }
 
 template <int NW, int TN, int STAGES>
@@ -436,8 +523,8 @@ static void launch_bf16_argmax(const GemmArgs& a, hipStream_t s) {
     hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, STAGES, kEpiArgmax, TN, true>), grid, block, 0,
                        s, a);
   else
-    hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, STAGES, kEpiArgmax, TN, (TN == 1)>), grid,
-                       block, 0, s, a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, STAGES, kEpiArgmax, TN, (TN == 1), (TN == 2)>),
+                       grid, block, 0, s, a);
 }
 
 static hipError_t launch_gemm_any(bool bf16, int epi, const GemmArgs& a, GemmPlan plan,
