@@ -211,6 +211,26 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
                            int64_t kv_cap, const int32_t* tokens, void* hidden, void* ws,
                            size_t ws_bytes, hdf_stream_t stream);
 
+/* Paged KV cache: the same drafter step over a cache whose rows are a pool of
+ * kv_pages pages of 64 rows, [n_layers][n_heads][kv_pages][64*head_dim] with the tile
+ * layout above (one page = one tile).  Context position i of sequence s lives in row
+ * i%64 of page page_table[s*max_pages + i/64], so a sequence grows by taking any free
+ * page and no sequence needs a contiguous slot (the serving loop that appends the
+ * n_s + 1 accepted positions of every round, Sec. 1).
+ * page_table  [n_seq][max_pages] int32 (device): pages 0 .. ceil(T_s/64)-1 of every
+ *             sequence must be valid page indices in [0, kv_pages) and no page may be
+ *             listed twice among the pages written by this call (new rows); entries
+ *             past a sequence's last page are not read.  Not checked on the device.
+ * max_pages   host: row stride of page_table; max_pages * 64 >= max_ctx
+ * kv_pages    host: pages in the pool (kv_pages * 64 < 2^31)
+ * Every other argument and limit is that of hdf_draft_block. */
+hdf_status hdf_draft_block_paged(const hdf_drafter* w, int n_seq, int B, const int32_t* ctx_len,
+                                 int max_ctx, const void* y_new, const int32_t* new_offsets,
+                                 int64_t n_new, const int32_t* page_table, int max_pages,
+                                 void* kv_k, void* kv_vt, int64_t kv_pages,
+                                 const int32_t* tokens, void* hidden, void* ws, size_t ws_bytes,
+                                 hdf_stream_t stream);
+
 /* ------------------------------------------------------------------------------
  * 3. LM head with fused greedy argmax (Sec. 2.3: z_k are the draft logits).
  *

@@ -263,11 +263,15 @@ size_t hdf_draft_block_workspace(const hdf_drafter* w, int n_seq, int B, int64_t
   return plan_workspace(*w, n_seq, B, n_new, max_ctx).total;
 }
 
-hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t* ctx_len,
-                           int max_ctx, const void* y_new, const int32_t* new_offsets,
-                           int64_t n_new, const int32_t* kv_offsets, void* kv_k, void* kv_vt,
-                           int64_t kv_cap, const int32_t* tokens, void* hidden, void* ws,
-                           size_t ws_bytes, hdf_stream_t stream) {
+// Both cache forms: kv_offsets (contiguous slots) or page_table (pages of 64 rows; the
+// cache then holds kv_cap / 64 pages).
+static hdf_status draft_block_impl(const hdf_drafter* w, int n_seq, int B, const int32_t* ctx_len,
+                                   int max_ctx, const void* y_new, const int32_t* new_offsets,
+                                   int64_t n_new, const int32_t* kv_offsets,
+                                   const int32_t* page_table, int max_pages, void* kv_k,
+                                   void* kv_vt, int64_t kv_cap, const int32_t* tokens,
+                                   void* hidden, void* ws, size_t ws_bytes,
+                                   hdf_stream_t stream) {
   hdf_status st = validate_drafter(w);
   if (st != HDF_OK) return st;
   if (n_seq < 0) return fail(HDF_E_INVALID, "draft_block: n_seq < 0");
@@ -275,11 +279,17 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
   if (max_ctx < 0 || n_new < 0) return fail(HDF_E_INVALID, "draft_block: negative size");
   if (kv_cap < 0 || kv_cap % 64 != 0)
     return fail(HDF_E_INVALID, "draft_block: kv_cap must be a non-negative multiple of 64");
+  if (kv_cap > INT32_MAX)
+    return fail(HDF_E_UNSUPPORTED, "draft_block: cache rows beyond 2^31 - 1");
+  if (page_table != nullptr && int64_t(max_pages) * 64 < max_ctx)
+    return fail(HDF_E_INVALID, "draft_block: max_pages=%d cannot hold max_ctx=%d", max_pages,
+                max_ctx);
   if (w->rope_cs != nullptr && int64_t(max_ctx) + B > w->rope_max_pos)
     return fail(HDF_E_INVALID, "draft_block: max_ctx + B exceeds the RoPE table (%d)",
                 w->rope_max_pos);
   if (n_seq == 0) return ok();
-  if (ctx_len == nullptr || kv_offsets == nullptr || tokens == nullptr || hidden == nullptr)
+  if (ctx_len == nullptr || (kv_offsets == nullptr && page_table == nullptr) ||
+      tokens == nullptr || hidden == nullptr)
     return fail(HDF_E_INVALID, "draft_block: null pointer");
   if (n_new > 0 && (y_new == nullptr || new_offsets == nullptr))
     return fail(HDF_E_INVALID, "draft_block: null y_new/new_offsets with n_new > 0");
@@ -329,6 +339,7 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
     hdf::PrepArgs pa{};
     pa.y = y_new; pa.r0 = r0; pa.n_ctx = rows; pa.ctx_gamma = w->ctx_norm; pa.c = cbuf;
     pa.ctx_len = ctx_len; pa.new_offsets = new_offsets; pa.kv_offsets = kv_offsets;
+    pa.page_table = page_table; pa.max_pages = max_pages;
     pa.n_seq = n_seq; pa.plan_pos = plan_pos; pa.plan_row = plan_row;
     pa.n_blk = block ? M : 0; pa.tokens = tokens; pa.emb = w->tok_emb;
     pa.attn_gamma = w->attn_norm[0]; pa.h = h; pa.u = u;
@@ -416,6 +427,7 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
     aa.kc = static_cast<char*>(kv_k) + l * layer_kv;
     aa.vtc = static_cast<char*>(kv_vt) + l * layer_kv;
     aa.cap = kv_cap; aa.kv_offsets = kv_offsets; aa.ctx_len = ctx_len;
+    aa.page_table = page_table; aa.max_pages = max_pages;
     aa.kb = kb; aa.vtb = vtb; aa.capb = capb;
     aa.n_seq = n_seq; aa.nh = nh; aa.hd = hd; aa.B = B; aa.QB = ((B + 15) / 16) * 16;
     aa.n_chunks = n_chunks; aa.chunk_len = P.chunk_len;
@@ -443,6 +455,33 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
   }
 #undef HDF_TRY
   return ok();
+}
+
+hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t* ctx_len,
+                           int max_ctx, const void* y_new, const int32_t* new_offsets,
+                           int64_t n_new, const int32_t* kv_offsets, void* kv_k, void* kv_vt,
+                           int64_t kv_cap, const int32_t* tokens, void* hidden, void* ws,
+                           size_t ws_bytes, hdf_stream_t stream) {
+  if (n_seq > 0 && kv_offsets == nullptr) return fail(HDF_E_INVALID, "draft_block: null kv_offsets");
+  return draft_block_impl(w, n_seq, B, ctx_len, max_ctx, y_new, new_offsets, n_new, kv_offsets,
+                          nullptr, 0, kv_k, kv_vt, kv_cap, tokens, hidden, ws, ws_bytes, stream);
+}
+
+hdf_status hdf_draft_block_paged(const hdf_drafter* w, int n_seq, int B, const int32_t* ctx_len,
+                                 int max_ctx, const void* y_new, const int32_t* new_offsets,
+                                 int64_t n_new, const int32_t* page_table, int max_pages,
+                                 void* kv_k, void* kv_vt, int64_t kv_pages,
+                                 const int32_t* tokens, void* hidden, void* ws, size_t ws_bytes,
+                                 hdf_stream_t stream) {
+  if (n_seq > 0 && page_table == nullptr)
+    return fail(HDF_E_INVALID, "draft_block_paged: null page_table");
+  if (max_pages < 0) return fail(HDF_E_INVALID, "draft_block_paged: max_pages < 0");
+  if (kv_pages < 0 || kv_pages > INT32_MAX / 64)
+    return fail(HDF_E_INVALID, "draft_block_paged: kv_pages=%lld outside [0, 2^25)",
+                static_cast<long long>(kv_pages));
+  return draft_block_impl(w, n_seq, B, ctx_len, max_ctx, y_new, new_offsets, n_new, nullptr,
+                          page_table, max_pages, kv_k, kv_vt, kv_pages * 64, tokens, hidden, ws,
+                          ws_bytes, stream);
 }
 
 size_t hdf_packed_weight_bytes(int N, int K, hdf_dtype dtype) {

@@ -7,9 +7,10 @@
 // Layouts (one layer): keys and values of a head in 64-row tiles, each tile in the
 // operand order of the MFMA instructions below (kc_offset / vc_offset), so a 64-key
 // tile of one head is 16 KB of contiguous keys plus 16 KB of contiguous values and
-// every operand load is a contiguous 1 KB per wave.  The context of sequence s starts at cache row kv_offsets[s] (a multiple
-// of 64); its block keys sit in 64-row slot s of separate block buffers of the
-// same layout.
+// every operand load is a contiguous 1 KB per wave.  The context of sequence s starts
+// at cache row kv_offsets[s] (a multiple of 64), or, in a paged cache, its tile j is
+// page page_table[s][j]; its block keys sit in 64-row slot s of separate block buffers
+// of the same layout.
 //
 // bf16 kernel: grid (context chunk + 1 block chunk, head, sequence x 16-query
 // group), 4 waves.  A wave streams 64-key tiles and keeps its 16 queries' state
@@ -53,22 +54,31 @@ attn_bf16_kernel(AttnArgs a) {
   const int ql = lane & 15;      // query within the group / row within a sub-tile
   const int T = a.ctx_len[s];
 
-  const bf16_t* kbase;
-  const bf16_t* vbase;  // first value tile of the segment
+  // 64-row tiles of this head's keys (values): tile j of the segment is tile
+  // tile0 + j, or page pt[j] of a paged cache.
+  const bf16_t* khead;
+  const bf16_t* vhead;
+  const int32_t* pt = nullptr;
+  int64_t tile0 = 0;
   int k_lo, k_hi;
   if (chunk < a.n_chunks) {
     k_lo = chunk * a.chunk_len;
     if (k_lo >= T) return;  // nothing of this sequence in this chunk
     k_hi = min(T, k_lo + a.chunk_len);
-    const int64_t row0 = a.kv_offsets[s];
-    kbase = static_cast<const bf16_t*>(a.kc) + (int64_t(h) * a.cap + row0) * HD;
-    vbase = static_cast<const bf16_t*>(a.vtc) + (int64_t(h) * (a.cap / 64) + row0 / 64) * HD * 64;
+    khead = static_cast<const bf16_t*>(a.kc) + int64_t(h) * a.cap * HD;
+    vhead = static_cast<const bf16_t*>(a.vtc) + int64_t(h) * a.cap * HD;
+    if (a.page_table != nullptr)
+      pt = a.page_table + int64_t(s) * a.max_pages;
+    else
+      tile0 = a.kv_offsets[s] >> 6;
   } else {
     k_lo = 0;
     k_hi = a.B;
-    kbase = static_cast<const bf16_t*>(a.kb) + (int64_t(h) * a.capb + int64_t(s) * 64) * HD;
-    vbase = static_cast<const bf16_t*>(a.vtb) + (int64_t(h) * (a.capb / 64) + s) * HD * 64;
+    khead = static_cast<const bf16_t*>(a.kb) + int64_t(h) * a.capb * HD;
+    vhead = static_cast<const bf16_t*>(a.vtb) + int64_t(h) * a.capb * HD;
+    tile0 = s;
   }
+  auto tile_of = [&](int t) -> int64_t { return pt != nullptr ? int64_t(pt[t >> 6]) : tile0 + (t >> 6); };
 
   // Q^T operand: lane holds Q[query ql][32j + 8g .. +7].
   const int q = qg * 16 + ql;
@@ -88,11 +98,15 @@ attn_bf16_kernel(AttnArgs a) {
   float m_run = -INFINITY;
   float l_run = 0.f;
 
+  // The tile of the next iteration is looked up one iteration ahead.
+  int64_t tile = (k_lo + wid * kKeyTile < k_hi) ? tile_of(k_lo + wid * kKeyTile) : 0;
   for (int t0 = k_lo + wid * kKeyTile; t0 < k_hi; t0 += kAttnWaves * kKeyTile) {
+    const int tn = t0 + kAttnWaves * kKeyTile;
+    const int64_t tile_next = tn < k_hi ? tile_of(tn) : 0;
     // K operands of the four 16-key sub-tiles: sub-tile st = 2*ks + p, row r -> key
     // t0 + 32ks + 8(r/4) + 4p + r%4 (the order of the cache tile layout).
     // In the cache tile layout each operand is 64 lanes x 16 contiguous bytes.
-    const bf16_t* ktile = kbase + int64_t(t0) * HD + lane * 8;
+    const bf16_t* ktile = khead + tile * 64 * HD + lane * 8;
     bf16x8_t kf[4][NJ];
 #pragma unroll
     for (int st = 0; st < 4; ++st)
@@ -100,7 +114,7 @@ attn_bf16_kernel(AttnArgs a) {
       for (int j = 0; j < NJ; ++j)
         kf[st][j] = __builtin_bit_cast(bf16x8_t, ld16(ktile + (st * NJ + j) * 512));
     // V^T operands: lane holds V^T[16dt + ql][t0 + 32ks + 8g .. +7].
-    const bf16_t* vtile = vbase + int64_t(t0 >> 6) * HD * 64 + lane * 8;
+    const bf16_t* vtile = vhead + tile * 64 * HD + lane * 8;
     u32x4 vf[2][NDT];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
@@ -185,6 +199,7 @@ attn_bf16_kernel(AttnArgs a) {
         oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pf_lo, oacc[dt], 0, 0, 0);
       }
     }
+    tile = tile_next;
   }
 
   // Wave -> LDS: lane (g, ql) holds O^T[16dt + 4g + i][ql].
@@ -306,22 +321,29 @@ __global__ void attn_f32_kernel(AttnArgs a, float* __restrict__ out) {
   for (int i = 0; i < hd; ++i) o[i] = 0.f;
   float m = -INFINITY, l = 0.f;
   for (int seg = 0; seg < 2; ++seg) {
-    const float* K;
-    const float* Vt;  // first value tile of the segment
+    const float* K;    // this head's keys and values
+    const float* Vt;
+    const int32_t* pt = nullptr;
+    int64_t row0 = 0;  // cache row of the segment's first key (contiguous layouts)
     int n;
     if (seg == 0) {
-      const int64_t row0 = a.kv_offsets[s];
-      K = static_cast<const float*>(a.kc) + (int64_t(h) * a.cap + row0) * hd;
-      Vt = static_cast<const float*>(a.vtc) + (int64_t(h) * (a.cap / 64) + row0 / 64) * hd * 64;
+      K = static_cast<const float*>(a.kc) + int64_t(h) * a.cap * hd;
+      Vt = static_cast<const float*>(a.vtc) + int64_t(h) * a.cap * hd;
+      if (a.page_table != nullptr)
+        pt = a.page_table + int64_t(s) * a.max_pages;
+      else
+        row0 = a.kv_offsets[s];
       n = a.ctx_len[s];
     } else {
-      K = static_cast<const float*>(a.kb) + (int64_t(h) * a.capb + int64_t(s) * 64) * hd;
-      Vt = static_cast<const float*>(a.vtb) + (int64_t(h) * (a.capb / 64) + s) * hd * 64;
+      K = static_cast<const float*>(a.kb) + int64_t(h) * a.capb * hd;
+      Vt = static_cast<const float*>(a.vtb) + int64_t(h) * a.capb * hd;
+      row0 = int64_t(s) * 64;
       n = a.B;
     }
     for (int j = 0; j < n; ++j) {
+      const int64_t row = pt != nullptr ? int64_t(pt[j >> 6]) * 64 + (j & 63) : row0 + j;
       float sc = 0.f;
-      for (int i = 0; i < hd; ++i) sc = fmaf(Q[i], K[kc_index(j, i, hd)], sc);
+      for (int i = 0; i < hd; ++i) sc = fmaf(Q[i], K[kc_index(row, i, hd)], sc);
       sc *= scale;
       const float mn = fmaxf(m, sc);
       const float al = expf(m - mn);
@@ -329,7 +351,7 @@ __global__ void attn_f32_kernel(AttnArgs a, float* __restrict__ out) {
       l = l * al + p;
 #pragma unroll
       for (int i = 0; i < hd; ++i)
-        o[i] = o[i] * al + p * Vt[vc_index(j, i, hd)];
+        o[i] = o[i] * al + p * Vt[vc_index(row, i, hd)];
       m = mn;
     }
   }

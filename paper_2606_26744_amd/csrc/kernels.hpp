@@ -105,6 +105,8 @@ struct PrepArgs {
   const int32_t* ctx_len;
   const int32_t* new_offsets;
   const int32_t* kv_offsets;
+  const int32_t* page_table;   // paged cache: [n_seq][max_pages] page of each 64-row tile, or NULL
+  int max_pages;
   int n_seq;
   int32_t* plan_pos;
   int32_t* plan_row;
@@ -136,7 +138,9 @@ struct AttnArgs {
   const void* kc;            // layer's context keys   [nh][cap][hd]
   const void* vtc;           // layer's context values [nh][hd][cap]
   int64_t cap;
-  const int32_t* kv_offsets; // [n_seq+1] cache slot of each sequence
+  const int32_t* kv_offsets; // [n_seq+1] cache slot of each sequence (contiguous cache)
+  const int32_t* page_table; // [n_seq][max_pages] page of each 64-row tile (paged cache), or NULL
+  int max_pages;
   const int32_t* ctx_len;    // [n_seq]
   const void* kb;            // block keys   [nh][capb][hd], slot s at row 64*s
   const void* vtb;           // block values [nh][hd][capb]

@@ -80,7 +80,9 @@ prep_kernel(PrepArgs a) {
       const int ns = a.new_offsets[lo + 1] - a.new_offsets[lo];
       const int pos = a.ctx_len[lo] - ns + int(r - a.new_offsets[lo]);
       a.plan_pos[r] = pos;
-      a.plan_row[r] = a.kv_offsets[lo] + pos;
+      a.plan_row[r] = a.page_table != nullptr
+                          ? a.page_table[int64_t(lo) * a.max_pages + (pos >> 6)] * 64 + (pos & 63)
+                          : a.kv_offsets[lo] + pos;
     }
     x = static_cast<const T*>(a.y) + r * a.d;
     gamma = a.ctx_gamma;

@@ -24,6 +24,7 @@ STATUS = {0: "HDF_OK", 1: "HDF_E_INVALID", 2: "HDF_E_UNSUPPORTED", 3: "HDF_E_WOR
 EXPORTS = ("hdf_last_error", "hdf_version", "hdf_hc_reduce", "hdf_rope_table",
            "hdf_packed_weight_bytes", "hdf_pack_weight",
            "hdf_kv_cache_bytes", "hdf_draft_block_workspace", "hdf_draft_block",
+           "hdf_draft_block_paged",
            "hdf_lm_head_workspace", "hdf_lm_head_argmax", "hdf_accept")
 
 
@@ -85,6 +86,9 @@ def lib() -> ctypes.CDLL:
     L.hdf_draft_block.restype = _I
     L.hdf_draft_block.argtypes = [ctypes.POINTER(Drafter), _I, _I, _P, _I, _P, _P, _I64, _P, _P, _P,
                                   _I64, _P, _P, _P, _SZ, _P]
+    L.hdf_draft_block_paged.restype = _I
+    L.hdf_draft_block_paged.argtypes = [ctypes.POINTER(Drafter), _I, _I, _P, _I, _P, _P, _I64, _P,
+                                        _I, _P, _P, _I64, _P, _P, _P, _SZ, _P]
     L.hdf_lm_head_workspace.restype = _SZ
     L.hdf_lm_head_workspace.argtypes = [_I64, _I]
     L.hdf_lm_head_argmax.restype = _I
@@ -292,18 +296,35 @@ class DrafterHandle:
                 torch.zeros(shape, dtype=self.torch_dtype, device=device))
 
     def draft_block(self, *, ctx_len: torch.Tensor, max_ctx: int, y_new: torch.Tensor,
-                    new_offsets: torch.Tensor, kv_offsets: torch.Tensor, kv_k: torch.Tensor,
-                    kv_vt: torch.Tensor, tokens: torch.Tensor, hidden: Optional[torch.Tensor] = None,
-                    ws: Optional[torch.Tensor] = None, stream=None):
+                    new_offsets: torch.Tensor, kv_k: torch.Tensor, kv_vt: torch.Tensor,
+                    tokens: torch.Tensor, kv_offsets: Optional[torch.Tensor] = None,
+                    page_table: Optional[torch.Tensor] = None,
+                    hidden: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                    stream=None):
+        """hdf_draft_block over a contiguous cache (kv_offsets [n_seq+1]) or
+        hdf_draft_block_paged over a paged one (page_table [n_seq][max_pages])."""
+        if (kv_offsets is None) == (page_table is None):
+            raise ValueError("give exactly one of kv_offsets and page_table")
         n_seq, B = tokens.shape
         n_new = y_new.shape[0]
-        kv_cap = kv_k.shape[2] * 64
         dev = tokens.device
         if hidden is None:
             hidden = torch.empty((n_seq * B, self.d), dtype=self.torch_dtype, device=dev)
         need = self.workspace_bytes(n_seq, B, n_new, max_ctx)
         if ws is None or ws.numel() < need:
             ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        if page_table is not None:
+            if page_table.dtype != torch.int32 or page_table.dim() != 2 or \
+                    page_table.shape[0] != n_seq or not page_table.is_contiguous():
+                raise ValueError("page_table must be a contiguous int32 [n_seq][max_pages] tensor")
+            _dev(ctx_len, y_new, new_offsets, page_table, kv_k, kv_vt, tokens, hidden, ws)
+            _check(lib().hdf_draft_block_paged(
+                ctypes.byref(self.s), n_seq, B, _ptr(ctx_len), max_ctx, _ptr(y_new),
+                _ptr(new_offsets), n_new, _ptr(page_table), page_table.shape[1], _ptr(kv_k),
+                _ptr(kv_vt), kv_k.shape[2], _ptr(tokens), _ptr(hidden), _ptr(ws), ws.numel(),
+                _stream(stream)))
+            return hidden
+        kv_cap = kv_k.shape[2] * 64
         _dev(ctx_len, y_new, new_offsets, kv_offsets, kv_k, kv_vt, tokens, hidden, ws)
         _check(lib().hdf_draft_block(ctypes.byref(self.s), n_seq, B, _ptr(ctx_len), max_ctx,
                                      _ptr(y_new), _ptr(new_offsets), n_new, _ptr(kv_offsets),
@@ -369,6 +390,31 @@ def read_kv_rows(kv_k: torch.Tensor, kv_vt: torch.Tensor, layer: int, row0: int,
         off0 = row0 - t_lo * 64
         res.append(rows[off0:off0 + n].contiguous())
     return res[0], res[1]
+
+
+def write_kv_rows_paged(kv_k: torch.Tensor, kv_vt: torch.Tensor, layer: int, pages: Sequence[int],
+                        k_rows: torch.Tensor, v_rows: torch.Tensor):
+    """Copies keys/values of positions 0..n-1 of one sequence into its pages (position i
+    goes to row i%64 of page pages[i//64]) of one layer.  Layout conversion only."""
+    n = k_rows.shape[0]
+    for j in range((n + 63) // 64):
+        lo, hi = 64 * j, min(n, 64 * j + 64)
+        write_kv_rows(kv_k, kv_vt, layer, int(pages[j]) * 64, k_rows[lo:hi], v_rows[lo:hi])
+
+
+def read_kv_rows_paged(kv_k: torch.Tensor, kv_vt: torch.Tensor, layer: int, pages: Sequence[int],
+                       n: int):
+    """Keys/values of positions 0..n-1 of one sequence, stored in `pages`, as [n, nh*hd]."""
+    ks, vs = [], []
+    for j in range((n + 63) // 64):
+        k, v = read_kv_rows(kv_k, kv_vt, layer, int(pages[j]) * 64, min(64, n - 64 * j))
+        ks.append(k)
+        vs.append(v)
+    if not ks:
+        d = kv_k.shape[1] * (kv_k.shape[3] // 64)
+        e = torch.empty((0, d), dtype=kv_k.dtype, device=kv_k.device)
+        return e, e.clone()
+    return torch.cat(ks), torch.cat(vs)
 
 
 def kv_slot_offsets(ctx_lens: Sequence[int]) -> list:

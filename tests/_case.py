@@ -19,7 +19,7 @@ class DraftCase:
     last ones); the rows before come from a synthetic already-filled cache."""
 
     def __init__(self, wl, ctx, new, *, B=None, random_norms=True, rope=True, sub=0,
-                 max_ctx=None, y_from=None):
+                 max_ctx=None, y_from=None, paged=False, spare_pages=0):
         self.wl = wl = dataclasses.replace(wl, n_seq=len(ctx), ctx_lens=list(ctx),
                                            block=B or wl.block)
         dr = wl.drafter
@@ -35,9 +35,29 @@ class DraftCase:
                                    rope_theta=theta, rope_max_pos=self.max_ctx + self.B)
         self.theta = theta
         offs = hdf.kv_slot_offsets(self.ctx)
-        self.kv_offsets = torch.tensor(offs, dtype=torch.int32, device=dev)
-        self.cap = offs[-1]
-        self.kv_k, self.kv_vt = self.h.alloc_kv(max(self.cap, 64))
+        self.paged = paged
+        if paged:
+            # A pool with spare pages; every sequence gets pages at random places of it
+            # (seeded), so no sequence's rows are contiguous.
+            need = [(t + 63) // 64 for t in self.ctx]
+            n_pages = sum(need) + spare_pages
+            perm = np.random.default_rng(1000 + sub).permutation(n_pages).tolist()
+            self.pages, k = [], 0
+            for n in need:
+                self.pages.append(perm[k:k + n])
+                k += n
+            self.max_pages = max(max(need), (self.max_ctx + 63) // 64)
+            pt = np.full((len(self.ctx), self.max_pages), -1, dtype=np.int32)
+            for s_, pg in enumerate(self.pages):
+                pt[s_, :len(pg)] = pg
+            self.page_table = torch.as_tensor(pt).to(dev)
+            self.kv_offsets = None
+            self.kv_k, self.kv_vt = self.h.alloc_kv(max(n_pages, 1) * 64)
+        else:
+            self.page_table = None
+            self.kv_offsets = torch.tensor(offs, dtype=torch.int32, device=dev)
+            self.cap = offs[-1]
+            self.kv_k, self.kv_vt = self.h.alloc_kv(max(self.cap, 64))
         self.ctx_len = torch.tensor(self.ctx, dtype=torch.int32, device=dev)
         nh, hd, L = dr.n_heads, dr.head_dim, dr.n_layers
         self.prefix = []
@@ -47,7 +67,10 @@ class DraftCase:
             for l in range(L):
                 if t0 > 0:
                     k, v = synth.kv_prefix(wl, t0, l, device=dev, sub=sub * 1000 + s)
-                    hdf.write_kv_rows(self.kv_k, self.kv_vt, l, offs[s], k, v)
+                    if paged:
+                        hdf.write_kv_rows_paged(self.kv_k, self.kv_vt, l, self.pages[s], k, v)
+                    else:
+                        hdf.write_kv_rows(self.kv_k, self.kv_vt, l, offs[s], k, v)
                     per_layer.append((bits(k), bits(v)))
                 else:
                     per_layer.append((np.zeros((0, dr.d)), np.zeros((0, dr.d))))
@@ -64,8 +87,15 @@ class DraftCase:
     def run(self, hidden=None, ws=None):
         return self.h.draft_block(ctx_len=self.ctx_len, max_ctx=self.max_ctx, y_new=self.y_new,
                                   new_offsets=self.new_offsets, kv_offsets=self.kv_offsets,
-                                  kv_k=self.kv_k, kv_vt=self.kv_vt, tokens=self.tokens,
-                                  hidden=hidden, ws=ws)
+                                  page_table=self.page_table, kv_k=self.kv_k, kv_vt=self.kv_vt,
+                                  tokens=self.tokens, hidden=hidden, ws=ws)
+
+    def read_cache(self, s, layer):
+        """Keys and values of positions 0..T_s-1 of sequence s, as [T_s, d] tensors."""
+        T = self.ctx[s]
+        if self.paged:
+            return hdf.read_kv_rows_paged(self.kv_k, self.kv_vt, layer, self.pages[s], T)
+        return hdf.read_kv_rows(self.kv_k, self.kv_vt, layer, int(self.kv_offsets[s]), T)
 
     def oracle_weights(self):
         dr = self.wl.drafter

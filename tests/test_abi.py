@@ -117,3 +117,43 @@ def test_kv_tile_layout_roundtrip():
         # key (row r, dim i) of head h sits at kv_k[0, h, tile, k_off[r, i]]
         assert kv_k[0, 1, 1, k_off[5, 7]] == k[5, hd + 7]
         assert kv_vt[0, 2, 2, v_off[3, hd - 1]] == v[64 + 3, 2 * hd + hd - 1]
+
+
+def _fake_drafter(L_layers=1, d=256, nh=4, hd=64):
+    fake = ctypes.c_void_p(4096)
+    arr = (ctypes.c_void_p * L_layers)(*([4096] * L_layers))
+    w = hdf.Drafter()
+    w.n_layers, w.d, w.n_heads, w.head_dim, w.d_ff, w.vocab = L_layers, d, nh, hd, 512, 1000
+    w.dtype, w.eps = hdf.HDF_BF16, 1e-6
+    w.tok_emb = fake
+    w.ctx_norm = None
+    for f in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down"):
+        setattr(w, f, ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p)))
+    w.final_norm = None
+    w.rope_cs = None
+    w.rope_max_pos = 0
+    return w, arr
+
+
+def test_draft_block_paged_validation():
+    """The paged entry point rejects a missing page table, a table too narrow for
+    max_ctx and an out-of-range page count before any launch; n_seq = 0 is a no-op."""
+    L = hdf.lib()
+    w, keep = _fake_drafter()
+    fake = ctypes.c_void_p(4096)
+    ws = 1 << 30
+
+    def call(page_table, max_pages, kv_pages, n_seq=2, max_ctx=100):
+        return _status(L.hdf_draft_block_paged(ctypes.byref(w), n_seq, 16, fake, max_ctx, fake,
+                                               fake, 8, page_table, max_pages, fake, fake,
+                                               kv_pages, fake, fake, fake, ws, None))
+    assert call(None, 4, 8) == "HDF_E_INVALID"                 # no page table
+    assert call(fake, 1, 8) == "HDF_E_INVALID"                 # 64 rows < max_ctx = 100
+    assert call(fake, -1, 8) == "HDF_E_INVALID"
+    assert call(fake, 4, 1 << 25) == "HDF_E_INVALID"           # kv_pages * 64 >= 2^31
+    assert call(fake, 4, -1) == "HDF_E_INVALID"
+    assert call(None, 0, 0, n_seq=0, max_ctx=0) == "HDF_OK"
+    # the contiguous entry point still requires its offsets
+    st = L.hdf_draft_block(ctypes.byref(w), 2, 16, fake, 100, fake, fake, 8, None, fake, fake,
+                           128, fake, fake, fake, ws, None)
+    assert _status(st) == "HDF_E_INVALID"

@@ -32,7 +32,6 @@ def _compare(case, seqs=None, check_cache=True):
     else:
         assert_f32_rows_close(got, ref, "hidden")
     if check_cache:
-        offs = case.kv_offsets.tolist()
         dr = case.wl.drafter
         for s in seqs[:3]:
             T, n = case.ctx[s], case.new[s]
@@ -40,7 +39,7 @@ def _compare(case, seqs=None, check_cache=True):
                 continue
             kv = context_kv(W, as_f64(case.y_rows(s)), np.arange(T - n, T))
             for l in range(dr.n_layers):
-                kk, vv = hdf.read_kv_rows(case.kv_k, case.kv_vt, l, offs[s], T)
+                kk, vv = case.read_cache(s, l)
                 k, v = kk[T - n:], vv[T - n:]
                 if case.wl.dtype == "bf16":
                     assert_bf16_state_close(as_f64(bits(k.contiguous())), kv[l][0], "cache K")
@@ -117,6 +116,38 @@ def test_ragged_long_contexts_sampled():
     _compare(case, seqs=[1, 3])
     del case
     torch.cuda.empty_cache()
+
+
+def test_paged_cache_scattered_pages():
+    """Paged cache: every sequence's 64-row tiles sit at random pages of a shared pool
+    (with spare pages in between); warm and cold rows, ragged lengths, one and two
+    query groups."""
+    wl = synth.small_bf16()
+    ctx = [1, 63, 64, 65, 200, 513, 1030]
+    new = [1, 5, 64, 16, 0, 513, 7]
+    _compare(DraftCase(wl, ctx, new, B=20, sub=9, paged=True, spare_pages=11))
+
+
+def test_paged_cache_fp32_multilayer():
+    wl = synth.tiny_fp32()
+    wl.drafter = synth.DrafterShape(d=256, n_layers=2, n_heads=4, head_dim=64, d_ff=512,
+                                    vocab=500)
+    _compare(DraftCase(wl, [130, 9, 64], [10, 9, 64], sub=10, paged=True, spare_pages=3))
+
+
+def test_paged_matches_contiguous_full_size():
+    """The full-size warm step over a paged pool gives bit-identical block states to the
+    contiguous cache with the same rows (same kernels, only the tile addresses differ)."""
+    wl = synth.drafter_full()
+    a = DraftCase(wl, [2048] * 8, [16] * 8, random_norms=False, sub=11)
+    ha = a.run().clone()
+    del a
+    b = DraftCase(wl, [2048] * 8, [16] * 8, random_norms=False, sub=11, paged=True,
+                  spare_pages=5)
+    hb = b.run().clone()
+    del b
+    torch.cuda.empty_cache()
+    assert torch.equal(ha, hb)
 
 
 def test_determinism():
