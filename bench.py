@@ -46,6 +46,9 @@ def parse():
                     help="also time the 64-sequence ragged decode workload")
     ap.add_argument("--cold", action="store_true",
                     help="also time the cold step (every context row reduced and projected)")
+    ap.add_argument("--decode", type=int, default=0, metavar="R",
+                    help="also time R chained rounds of the paged decode loop (8 sequences "
+                         "from 2048 positions, n+1 committed positions appended per round)")
     ap.add_argument("--blas-ref", action="store_true",
                     help="also time the vendor BLAS (torch.matmul) on the matrix-core bound "
                          "GEMM shapes, for context")
@@ -151,6 +154,75 @@ def lm_head_m_sweep(torch, synth, hdf, h, d):
                     "mfma_frac": round(tf / BF16_PEAK_TFLOPS, 4), "GB/s": round(gbs, 1)})
         del hid, ws, am
     return out
+
+
+def decode_leg(torch, synth, hdf, rounds, warmup):
+    """Chained drafting rounds of the full-size drafter over the paged cache: 8
+    sequences whose first 2032 context positions are already cached (pages taken in a
+    shuffled order), a first round projecting the last 16, then one round after another
+    appending each sequence's n_s + 1 committed positions.  The target model is stood in
+    for by device-side tokens that copy each draft with probability 0.8.  Timed: the
+    rounds end to end, with the page bookkeeping and the per-round read of the
+    accepted lengths the host needs."""
+    import numpy as np
+    from paper_2606_26744_amd.decode import PagedDecoder
+    wl = synth.drafter_full()
+    dr = wl.drafter
+    n_seq, B = wl.n_seq, wl.block
+    T0 = int(wl.ctx_lens[0])
+    max_ctx = T0 + (warmup + rounds + 1) * B
+    w = synth.drafter_weights(wl, device="cuda")
+    h = hdf.DrafterHandle(w, n_layers=dr.n_layers, d=dr.d, n_heads=dr.n_heads,
+                          head_dim=dr.head_dim, d_ff=dr.d_ff, vocab=dr.vocab, eps=dr.eps,
+                          rope_theta=dr.rope_theta, rope_max_pos=max_ctx + B)
+    n_pages = n_seq * ((max_ctx + 63) // 64) + 8
+    order = np.random.default_rng(wl.seed).permutation(n_pages)
+    dec = PagedDecoder(h, n_seq, B, max_ctx, n_pages, n_seq * B, page_order=order)
+    pre = T0 - wl.new_rows
+    dec.preload(np.full(n_seq, pre, dtype=np.int64))     # the cached prefix of every sequence
+    for s in range(n_seq):
+        for l in range(dr.n_layers):
+            k, v = synth.kv_prefix(wl, pre, l, device="cuda", sub=s)
+            hdf.write_kv_rows_paged(dec.kv_k, dec.kv_vt, l, dec.pages[s], k, v)
+            del k, v
+    dec.set_anchors(synth.block_tokens(wl, device="cuda")[:, 0])
+    red = synth.reducer_inputs(wl, n_seq * B, device="cuda")
+    V, p = dr.vocab, 0.8
+    gen = torch.Generator(device="cuda").manual_seed(wl.seed)
+
+    def targets(drafts):
+        n, K = drafts.shape
+        u = torch.rand((n, K), generator=gen, device="cuda")
+        other = ((drafts.long() + 1 + torch.randint(0, V - 1, (n, K), generator=gen,
+                                                      device="cuda")) % V).to(torch.int32)
+        bonus = torch.randint(0, V, (n, 1), generator=gen, device="cuda").to(torch.int32)
+        return torch.cat([torch.where(u < p, drafts, other), bonus], dim=1).contiguous()
+
+    counts = np.full(n_seq, wl.new_rows, dtype=np.int64)
+
+    def one(counts):
+        n_new = int(counts.sum())
+        out = dec.round(red["H"][:n_new], counts, red["W_g"], red["b_g"], targets)
+        return dec.next_counts(out["accept_len"])
+
+    for _ in range(warmup):
+        counts = one(counts)
+    torch.cuda.synchronize()
+    committed = 0
+    t0 = time.perf_counter()
+    for _ in range(rounds):
+        counts = one(counts)
+        committed += int(counts.sum())
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    res = {"n_seq": n_seq, "rounds": rounds, "ms_per_round": round(dt / rounds * 1e3, 4),
+           "blocks_per_s": round(n_seq * rounds / dt, 1),
+           "committed_tokens_per_s": round(committed / dt, 1),
+           "mean_accept_len": round(committed / (rounds * n_seq) - 1, 3),
+           "context_end": [int(x) for x in dec.ctx], "pages_used": n_pages - dec.pool.free}
+    del dec, h, w, red
+    torch.cuda.empty_cache()
+    return res
 
 
 def blas_reference(torch):
@@ -358,7 +430,7 @@ def main():
         res["cpu_baseline"] = cpu_baseline(torch, synth, wl, h, w, red, args, offs)
     if a.blas_ref:
         res["blas_reference"] = blas_reference(torch)
-    if a.ragged or a.cold:
+    if a.ragged or a.cold or a.decode:
         del bufs, args
         torch.cuda.empty_cache()
     if a.ragged:
@@ -366,6 +438,8 @@ def main():
     if a.cold:
         res["drafter_full_cold"] = ragged_leg(torch, synth, hdf, max(a.steps // 5, 5), 3,
                                               synth.drafter_full_cold())
+    if a.decode:
+        res["paged_decode"] = decode_leg(torch, synth, hdf, a.decode, 5)
     print(json.dumps(res), flush=True)
 
 

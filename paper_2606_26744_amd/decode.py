@@ -87,6 +87,12 @@ class PagedDecoder:
     def set_anchors(self, anchors: torch.Tensor):
         self.tokens[:, 0] = anchors
 
+    def preload(self, counts: Sequence[int]):
+        """Takes pages for counts[s] more context positions of every sequence and counts
+        them as cached: for rows the caller writes into the pages itself (a prompt whose
+        keys and values were computed elsewhere)."""
+        self._grow(np.asarray(counts, dtype=np.int64))
+
     def _grow(self, new_counts: np.ndarray):
         self._copied.synchronize()          # the staging buffer is free again
         for s in range(self.n_seq):
