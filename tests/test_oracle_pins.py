@@ -17,6 +17,7 @@ from oracle.accept import accept
 from oracle.drafter import Weights, attention, block_forward, context_kv, draft_block, rope
 from oracle.lm_head import lm_head_argmax
 from oracle.reducer import hc_reduce
+from oracle.fc_reducer import fc_parameter_count, fc_reduce
 from oracle.step import drafter_step
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -202,6 +203,66 @@ def test_table1_parameter_counts():
     sols = [(mm, dd) for mm in range(1, 17) for dd in (2 ** k for k in range(6, 15))
             if (mm * mm * dd) // 1000 == 65 and (mm * dd * dd) // 10**6 == 67]
     assert sols == [(4, 4096)]
+
+
+def test_fc_reducer_parameter_count_is_table1():
+    """Table 1: the generic fc projection R^{md} -> R^d has about 67M parameters at the
+    m = 4, d = 4096 the gated reducer's 65K fixes."""
+    g = _load("table1_params.json")
+    n = fc_parameter_count(g["m"], g["d"])
+    assert g["fc_params_printed"] == f"{n // 10**6}M"
+    W = np.zeros((g["d"], g["m"] * g["d"]), dtype=np.float32)
+    assert W.size == n
+    fc_reduce(np.zeros((1, g["m"], g["d"])), W, dtype="f32")   # the oracle takes this shape
+
+
+def test_fc_block_identity_is_plain_path_sum():
+    """W_fc = [I I ... I] (one identity per path) collapses the paths by plain summation,
+    the same result as the gated reducer with every gate at 1."""
+    rng = np.random.default_rng(3)
+    n, m, d = 5, 4, 32
+    H = rng.standard_normal((n, m, d))
+    W = np.concatenate([np.eye(d)] * m, axis=1)
+    y = fc_reduce(H, W, dtype="f32")
+    np.testing.assert_allclose(y, nm.round_f32(H.sum(axis=1)), rtol=0, atol=1e-6)
+    # the gated reducer with saturated gates (large bias) agrees
+    y_g, _ = hc_reduce(H, np.zeros((m, m * d)), np.full(m, 40.0), dtype="f32")
+    np.testing.assert_allclose(y, y_g, rtol=1e-6, atol=1e-6)
+
+
+def test_fc_path_selector_and_bias():
+    """A W_fc that keeps only path j returns that path; the bias is added per feature."""
+    rng = np.random.default_rng(4)
+    n, m, d = 3, 3, 16
+    H = rng.standard_normal((n, m, d))
+    for j in range(m):
+        W = np.zeros((d, m * d))
+        W[:, j * d:(j + 1) * d] = np.eye(d)
+        b = np.arange(d, dtype=np.float64) * 0.5
+        np.testing.assert_allclose(fc_reduce(H, W, b, dtype="f32"),
+                                   nm.round_f32(H[:, j, :] + b), rtol=0, atol=1e-6)
+
+
+def test_fc_is_a_dense_linear_map_brute_force():
+    """Brute force on a tiny case: every output is the explicit double sum over paths
+    and features of W[o, j*d + c] * H[j, c]; and the map is linear in H."""
+    rng = np.random.default_rng(5)
+    n, m, d = 2, 2, 3
+    H = rng.standard_normal((n, m, d))
+    W = rng.standard_normal((d, m * d))
+    want = np.zeros((n, d))
+    for t in range(n):
+        for o in range(d):
+            acc = 0.0
+            for j in range(m):
+                for c in range(d):
+                    acc += W[o, j * d + c] * H[t, j, c]
+            want[t, o] = acc
+    np.testing.assert_array_equal(fc_reduce(H, W, dtype="f32"), nm.round_f32(want))
+    H2 = rng.standard_normal((n, m, d))
+    np.testing.assert_allclose(fc_reduce(2 * H - 3 * H2, W, dtype="f32"),
+                               2 * fc_reduce(H, W, dtype="f32") - 3 * fc_reduce(H2, W, dtype="f32"),
+                               rtol=1e-5, atol=1e-5)
 
 
 # --------------------------------------------------------------------------- RoPE / attention
