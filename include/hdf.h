@@ -3,6 +3,7 @@
  *
  * One decode round of HyperDFlash drafting (arxiv 2606.26744):
  *   1. hdf_hc_reduce       gated residual reducer, Eq. (1) of Sec. 2.2
+ *      (hdf_fc_reduce      the generic dense fc reducer, the fallback of Sec. 2.2)
  *   2. hdf_draft_block     one-pass DFlash block drafter over the reduced context
  *                          (Sec. 1, Sec. 2.1; slot alignment of Sec. 2.3)
  *   3. hdf_lm_head_argmax  draft logits z_k and greedy draft tokens (Sec. 2.3)
@@ -91,6 +92,27 @@ typedef struct {
 hdf_status hdf_hc_reduce(const void* H, const void* W_g, const float* b_g, int64_t n_tok,
                          int m, int d, hdf_dtype dtype, const hdf_reduce_params* params,
                          void* Y, float* alpha, hdf_stream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * 1b. Generic fc reducer, the fallback path collapse (Sec. 2.2, Table 1): a static
+ * dense projection of the flattened multi-path residual,
+ *     y_t = W_fc vec(H_t) (+ b_fc),   vec path-major (index j*d + c),
+ * with no normalisation (about 67M parameters at m = 4, d = 4096, against the gated
+ * reducer's 65K).  Accumulation in fp32, Y rounded to `dtype`.
+ * ----------------------------------------------------------------------------*/
+/* Workspace bytes of hdf_fc_reduce (0 on invalid arguments). */
+size_t hdf_fc_reduce_workspace(int64_t n_tok, int m, int d, hdf_dtype dtype);
+/* H     [n_tok][m][d] dtype
+ * W_fc  [d][m*d] dtype, packed (hdf_pack_weight with N = d, K = m*d)
+ * b_fc  [d] fp32 or NULL (no bias)
+ * Y     [n_tok][d] dtype (out)
+ * ws, ws_bytes  at least hdf_fc_reduce_workspace(...) bytes, 256-byte aligned; its
+ *       contents on entry do not matter.
+ * Limits: 1 <= m <= 8; d % 4 == 0; m*d a multiple of 64 (bf16) or 16 (fp32);
+ *         0 <= n_tok < 2^31 (0 is a no-op).  H, W_fc, Y 16-byte aligned. */
+hdf_status hdf_fc_reduce(const void* H, const void* W_fc, const float* b_fc, int64_t n_tok, int m,
+                         int d, hdf_dtype dtype, void* Y, void* ws, size_t ws_bytes,
+                         hdf_stream_t stream);
 
 /* ------------------------------------------------------------------------------
  * Weight layout of every projection and of the LM head.

@@ -214,6 +214,67 @@ hdf_status hdf_hc_reduce(const void* H, const void* W_g, const float* b_g, int64
   return ok();
 }
 
+// Generic fc reducer: rows are projected kFcChunk at a time, each chunk's split-K
+// partials summed (+ bias) and rounded by one row-wise pass.
+static constexpr int64_t kFcChunk = 16384;
+
+static bool fc_shape_ok(int m, int d, hdf_dtype dtype) {
+  if (dtype != HDF_F32 && dtype != HDF_BF16) return false;
+  if (m < 1 || m > 8 || d < 4 || d % 4 != 0) return false;
+  return (int64_t(m) * d) % hdf::gemm_k_align(dtype == HDF_BF16) == 0;
+}
+
+static size_t fc_parts_bytes(int64_t n_tok, int m, int d, hdf_dtype dtype) {
+  const int64_t rows = n_tok < kFcChunk ? n_tok : kFcChunk;
+  if (rows <= 0) return 0;
+  const hdf::GemmPlan pl = hdf::gemm_plan(dtype == HDF_BF16, int(rows), d, m * d);
+  return size_t(pl.splits) * size_t(rows) * size_t(d) * 4;
+}
+
+size_t hdf_fc_reduce_workspace(int64_t n_tok, int m, int d, hdf_dtype dtype) {
+  if (n_tok < 0 || !fc_shape_ok(m, d, dtype)) return 0;
+  return (fc_parts_bytes(n_tok, m, d, dtype) + 255) / 256 * 256;
+}
+
+hdf_status hdf_fc_reduce(const void* H, const void* W_fc, const float* b_fc, int64_t n_tok, int m,
+                         int d, hdf_dtype dtype, void* Y, void* ws, size_t ws_bytes,
+                         hdf_stream_t stream) {
+  if (dtype != HDF_F32 && dtype != HDF_BF16) return fail(HDF_E_INVALID, "fc_reduce: bad dtype");
+  if (n_tok < 0) return fail(HDF_E_INVALID, "fc_reduce: n_tok < 0");
+  if (m < 1 || m > 8) return fail(HDF_E_INVALID, "fc_reduce: m=%d outside [1, 8]", m);
+  if (!fc_shape_ok(m, d, dtype))
+    return fail(HDF_E_INVALID, "fc_reduce: d=%d (need d %% 4 == 0 and m*d a multiple of %d)", d,
+                hdf::gemm_k_align(dtype == HDF_BF16));
+  if (n_tok > INT32_MAX) return fail(HDF_E_UNSUPPORTED, "fc_reduce: n_tok beyond 2^31 - 1");
+  if (n_tok == 0) return ok();
+  if (H == nullptr || W_fc == nullptr || Y == nullptr)
+    return fail(HDF_E_INVALID, "fc_reduce: null pointer");
+  if (!aligned16(H) || !aligned16(W_fc) || !aligned16(Y))
+    return fail(HDF_E_INVALID, "fc_reduce: H, W_fc and Y must be 16-byte aligned");
+  const size_t need = fc_parts_bytes(n_tok, m, d, dtype);
+  if (ws == nullptr || ws_bytes < need)
+    return fail(HDF_E_WORKSPACE, "fc_reduce: workspace of %zu bytes needed, %zu given", need,
+                ws_bytes);
+  if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0)
+    return fail(HDF_E_INVALID, "fc_reduce: workspace must be 256-byte aligned");
+  const bool bf = dtype == HDF_BF16;
+  const size_t el = bf ? 2 : 4;
+  const int K = m * d;
+  const hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  float* parts = static_cast<float*>(ws);
+  for (int64_t r0 = 0; r0 < n_tok; r0 += kFcChunk) {
+    const int rows = int(n_tok - r0 < kFcChunk ? n_tok - r0 : kFcChunk);
+    const hdf::GemmPlan pl = hdf::gemm_plan(bf, rows, d, K);
+    hipError_t e = hdf::launch_gemm_partial(bf, static_cast<const char*>(H) + r0 * K * el, K, W_fc,
+                                            rows, d, K, pl, parts, s);
+    if (e != hipSuccess) return hip_fail(e, "fc_reduce gemm");
+    e = hdf::launch_split_sum_store(bf, parts, pl.splits, rows, d, b_fc,
+                                    static_cast<char*>(Y) + r0 * d * el, s);
+    if (e != hipSuccess) return hip_fail(e, "fc_reduce store");
+  }
+  return ok();
+}
+
 hdf_status hdf_accept(const int32_t* draft, int draft_stride, const int32_t* target, int n_seq,
                       int K, int32_t* accept_len, int32_t* next_anchor, int32_t* commit_offsets,
                       int32_t* commit_tokens, hdf_stream_t stream) {

@@ -128,6 +128,9 @@ hipError_t launch_qkv_epilogue(bool bf16, const QkvEpiArgs& a, hipStream_t s);
 // Two epilogues (context rows, block rows) in one launch.
 hipError_t launch_qkv_epilogue2(bool bf16, const QkvEpiArgs& a, const QkvEpiArgs& b,
                                 hipStream_t s);
+// out[M][N] = sum_z parts[z][M][N] (+ bias[N], may be NULL), rounded to the dtype; N % 4 == 0
+hipError_t launch_split_sum_store(bool bf16, const float* parts, int S, int64_t M, int N,
+                                  const float* bias, void* out, hipStream_t s);
 // act = SiLU(gate) * up from parts [S][M][2F] (gate columns first)
 hipError_t launch_silu_epilogue(bool bf16, const float* parts, int S, int64_t M, int F, void* act,
                                 hipStream_t s);

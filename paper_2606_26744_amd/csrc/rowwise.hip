@@ -301,6 +301,32 @@ silu_kernel(const float* __restrict__ parts, int S, int64_t M, int F, T* __restr
   }
 }
 
+// out = sum_z parts[z] (+ bias per column), rounded to the working dtype; rows of N
+// columns (N % 4 == 0), four consecutive columns per item.
+template <typename T>
+__global__ void __launch_bounds__(kRowThreads)
+split_sum_store_kernel(const float* __restrict__ parts, int S, int64_t M, int N,
+                       const float* __restrict__ bias, T* __restrict__ out) {
+  const int64_t n4 = M * N / 4;
+  const int64_t zs = M * N;
+  for (int64_t e = int64_t(blockIdx.x) * kRowThreads + threadIdx.x; e < n4;
+       e += int64_t(gridDim.x) * kRowThreads) {
+    const int64_t idx = e * 4;
+    const int c = int(idx % N);
+    float4 x = *reinterpret_cast<const float4*>(parts + idx);
+    for (int z = 1; z < S; ++z) {
+      const float4 t = *reinterpret_cast<const float4*>(parts + z * zs + idx);
+      x.x += t.x; x.y += t.y; x.z += t.z; x.w += t.w;
+    }
+    float o[4] = {x.x, x.y, x.z, x.w};
+    if (bias != nullptr) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[j] += bias[c + j];
+    }
+    store4<T>(out + idx, o);
+  }
+}
+
 // ---------------------------------------------------------------------------- host side
 
 hipError_t launch_prep(bool bf16, const PrepArgs& a, hipStream_t s) {
@@ -364,6 +390,21 @@ hipError_t launch_silu_epilogue(bool bf16, const float* parts, int S, int64_t M,
   else
     hipLaunchKernelGGL(silu_kernel<float>, dim3(unsigned(blocks)), dim3(kRowThreads), 0, s, parts, S,
                        M, F, static_cast<float*>(act));
+  return hipGetLastError();
+}
+
+hipError_t launch_split_sum_store(bool bf16, const float* parts, int S, int64_t M, int N,
+                                  const float* bias, void* out, hipStream_t s) {
+  const int64_t n4 = M * N / 4;
+  if (n4 <= 0) return hipSuccess;
+  int64_t blocks = (n4 + kRowThreads - 1) / kRowThreads;
+  if (blocks > 65536) blocks = 65536;
+  if (bf16)
+    hipLaunchKernelGGL(split_sum_store_kernel<bf16_t>, dim3(unsigned(blocks)), dim3(kRowThreads), 0,
+                       s, parts, S, M, N, bias, static_cast<bf16_t*>(out));
+  else
+    hipLaunchKernelGGL(split_sum_store_kernel<float>, dim3(unsigned(blocks)), dim3(kRowThreads), 0,
+                       s, parts, S, M, N, bias, static_cast<float*>(out));
   return hipGetLastError();
 }
 

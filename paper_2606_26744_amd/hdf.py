@@ -24,7 +24,7 @@ STATUS = {0: "HDF_OK", 1: "HDF_E_INVALID", 2: "HDF_E_UNSUPPORTED", 3: "HDF_E_WOR
 EXPORTS = ("hdf_last_error", "hdf_version", "hdf_hc_reduce", "hdf_rope_table",
            "hdf_packed_weight_bytes", "hdf_pack_weight",
            "hdf_kv_cache_bytes", "hdf_draft_block_workspace", "hdf_draft_block",
-           "hdf_draft_block_paged",
+           "hdf_draft_block_paged", "hdf_fc_reduce_workspace", "hdf_fc_reduce",
            "hdf_lm_head_workspace", "hdf_lm_head_argmax", "hdf_accept")
 
 
@@ -89,6 +89,10 @@ def lib() -> ctypes.CDLL:
     L.hdf_draft_block_paged.restype = _I
     L.hdf_draft_block_paged.argtypes = [ctypes.POINTER(Drafter), _I, _I, _P, _I, _P, _P, _I64, _P,
                                         _I, _P, _P, _I64, _P, _P, _P, _SZ, _P]
+    L.hdf_fc_reduce_workspace.restype = _SZ
+    L.hdf_fc_reduce_workspace.argtypes = [_I64, _I, _I, _I]
+    L.hdf_fc_reduce.restype = _I
+    L.hdf_fc_reduce.argtypes = [_P, _P, _P, _I64, _I, _I, _I, _P, _P, _SZ, _P]
     L.hdf_lm_head_workspace.restype = _SZ
     L.hdf_lm_head_workspace.argtypes = [_I64, _I]
     L.hdf_lm_head_argmax.restype = _I
@@ -147,6 +151,24 @@ def hc_reduce(H: torch.Tensor, W_g: torch.Tensor, b_g: torch.Tensor, *, eps: flo
     _check(lib().hdf_hc_reduce(_ptr(H), _ptr(W_g), _ptr(b_g), n, m, d, _dt(H), ctypes.byref(p),
                                _ptr(Y), _ptr(alpha), _stream(stream)))
     return Y, alpha
+
+
+def fc_reduce(H: torch.Tensor, W_fc: "PackedWeight", b_fc: Optional[torch.Tensor] = None, *,
+              Y: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None, stream=None):
+    """hdf_fc_reduce: H [n_tok, m, d], W_fc packed [d][m*d], b_fc [d] fp32 or None ->
+    Y [n_tok, d]."""
+    n, m, d = H.shape
+    if W_fc.N != d or W_fc.K != m * d:
+        raise ValueError("W_fc must be a packed [d][m*d] weight")
+    if Y is None:
+        Y = torch.empty((n, d), dtype=H.dtype, device=H.device)
+    need = int(lib().hdf_fc_reduce_workspace(n, m, d, _dt(H)))
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=H.device)
+    _dev(H, W_fc.data, b_fc, Y, ws)
+    _check(lib().hdf_fc_reduce(_ptr(H), W_fc.data_ptr(), _ptr(b_fc), n, m, d, _dt(H), _ptr(Y),
+                               _ptr(ws), ws.numel(), _stream(stream)))
+    return Y
 
 
 # ----------------------------------------------------------------------------- accept

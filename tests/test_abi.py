@@ -157,3 +157,22 @@ def test_draft_block_paged_validation():
     st = L.hdf_draft_block(ctypes.byref(w), 2, 16, fake, 100, fake, fake, 8, None, fake, fake,
                            128, fake, fake, fake, ws, None)
     assert _status(st) == "HDF_E_INVALID"
+
+
+def test_fc_reduce_validation():
+    L = hdf.lib()
+    fake = ctypes.c_void_p(4096)
+    ws = 1 << 30
+    call = lambda n, m, d, dt=1, H=fake: _status(L.hdf_fc_reduce(H, fake, None, n, m, d, dt, fake,
+                                                                 fake, ws, None))
+    assert call(-1, 4, 256) == "HDF_E_INVALID"
+    assert call(1, 0, 256) == "HDF_E_INVALID"
+    assert call(1, 9, 256) == "HDF_E_INVALID"
+    assert call(1, 1, 36) == "HDF_E_INVALID"          # m*d = 36: not a multiple of 64
+    assert call(1, 4, 256, H=None) == "HDF_E_INVALID"
+    assert call(0, 4, 256, H=None) == "HDF_OK"
+    assert L.hdf_fc_reduce_workspace(10, 4, 256, 1) > 0
+    assert L.hdf_fc_reduce_workspace(10, 4, 30, 1) == 0
+    # too small a workspace
+    st = L.hdf_fc_reduce(fake, fake, None, 10, 4, 256, 1, fake, fake, 16, None)
+    assert _status(st) == "HDF_E_WORKSPACE"
