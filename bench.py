@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--decode", type=int, default=0, metavar="R",
                     help="also time R chained rounds of the paged decode loop (8 sequences "
                          "from 2048 positions, n+1 committed positions appended per round)")
+    ap.add_argument("--fc-reducer", action="store_true",
+                    help="also time the generic fc reducer beside the gated one (warm-step "
+                         "rows and the reducer-stress shape)")
     ap.add_argument("--blas-ref", action="store_true",
                     help="also time the vendor BLAS (torch.matmul) on the matrix-core bound "
                          "GEMM shapes, for context")
@@ -223,6 +226,44 @@ def decode_leg(torch, synth, hdf, rounds, warmup):
     del dec, h, w, red
     torch.cuda.empty_cache()
     return res
+
+
+def fc_reducer_leg(torch, synth, hdf):
+    """The generic fc reducer (a dense m*d -> d projection, 67M parameters at m = 4,
+    d = 4096) beside the gated reducer on the same H: the full-size step's 128 new rows
+    and the 65536 x 4 x 7168 stress shape.  HIP events around 10 calls each."""
+    out = []
+    for name, wl, n in (("drafter_full rows", synth.drafter_full(), 128),
+                        ("reducer_stress", synth.reducer_stress(), None)):
+        n = n or wl.n_tok
+        ri = synth.reducer_inputs(wl, n, device="cuda")
+        m, d = wl.m, wl.d
+        W = synth.normal([d, m * d], wl.w_std, wl.seed, 73, dtype=wl.dtype, device="cuda")
+        Wp = hdf.pack_weight(W)
+        del W
+        Y = torch.empty((n, d), dtype=torch.bfloat16, device="cuda")
+        ws = torch.empty(max(int(hdf.lib().hdf_fc_reduce_workspace(n, m, d, hdf.HDF_BF16)), 1),
+                         dtype=torch.uint8, device="cuda")
+        row = {"case": name, "n_tok": n, "m": m, "d": d}
+        for kind, fn in (("gated", lambda: hdf.hc_reduce(ri["H"], ri["W_g"], ri["b_g"], Y=Y)),
+                         ("fc", lambda: hdf.fc_reduce(ri["H"], Wp, Y=Y, ws=ws))):
+            for _ in range(2):
+                fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(10):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            row[kind + "_us"] = round(e0.elapsed_time(e1) / 10 * 1e3, 1)
+        row["fc_params"] = m * d * d
+        row["gated_params"] = m * m * d + m
+        row["fc_TFLOP/s"] = round(2.0 * n * m * d * d / (row["fc_us"] * 1e-6) / 1e12, 1)
+        out.append(row)
+        del ri, Wp, Y, ws
+        torch.cuda.empty_cache()
+    return out
 
 
 def blas_reference(torch):
@@ -428,6 +469,8 @@ def main():
         del x, y
     if not a.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(torch, synth, wl, h, w, red, args, offs)
+    if a.fc_reducer:
+        res["fc_reducer"] = fc_reducer_leg(torch, synth, hdf)
     if a.blas_ref:
         res["blas_reference"] = blas_reference(torch)
     if a.ragged or a.cold or a.decode:
