@@ -8,6 +8,7 @@
  *                          (Sec. 1, Sec. 2.1; slot alignment of Sec. 2.3)
  *   3. hdf_lm_head_argmax  draft logits z_k and greedy draft tokens (Sec. 2.3)
  *   4. hdf_accept          greedy verification: longest agreeing prefix (Sec. 1, Sec. 3.4)
+ *      (hdf_sample_tokens, hdf_accept_sample: the same at temperature T > 0)
  *
  * Conventions shared by every call:
  *   - Tensor arguments are DEVICE pointers unless marked "host".  Tensors are dense,
@@ -299,6 +300,55 @@ hdf_status hdf_lm_head_argmax(const void* hidden, const void* W_lm, int64_t M, i
 hdf_status hdf_accept(const int32_t* draft, int draft_stride, const int32_t* target, int n_seq,
                       int K, int32_t* accept_len, int32_t* next_anchor, int32_t* commit_offsets,
                       int32_t* commit_tokens, hdf_stream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * 5. Temperature sampling and speculative-sampling verification (the temperature-1
+ * results of Tables 2 and 3).  The paper does not restate the verification rule;
+ * this is the standard one of speculative decoding: with p_i the target's and q_i
+ * the drafter's softmax(logits / T) at the position of draft i,
+ *     draft x_i is accepted with probability min(1, p_i(x_i) / q_i(x_i)), in order;
+ *     at the first rejection n the next token is drawn from max(0, p_n - q_n)
+ *     renormalised; after K acceptances it is drawn from p_K (the bonus token).
+ * Random numbers come from Philox4x64-10 (Salmon et al., SC'11) with key
+ * (seed, stream_id) and counter (row, v/4, purpose, 0); word v%4 of the block gives
+ * u = (its top 24 bits + 1/2) / 2^24.  Purpose 0: the noise of hdf_sample_tokens
+ * (row = logits row, v = token); 1: the acceptance uniform of draft i of sequence s
+ * (row = s, v = i); 2: the noise of the final draw of sequence s (row = s, v = token).
+ * Draws from softmax(x) are argmax_v (x_v - log(-log u_v)) (Gumbel-max).
+ * ----------------------------------------------------------------------------*/
+/* Workspace bytes of hdf_sample_tokens for `rows` rows (0 on invalid arguments). */
+size_t hdf_sample_workspace(int64_t rows, int vocab);
+/* logits  rows x vocab fp32, row r at logits + r*ld (e.g. the LM head's logits output)
+ * tokens  [rows] int32 (out, may be NULL): a draw from softmax(logits[r] / temperature)
+ * lse     [rows] fp32 (out, may be NULL): logsumexp(logits[r] / temperature)
+ * Limits: 0 <= rows <= 65535, vocab >= 1, ld >= vocab, 0 < temperature < inf; at least
+ * one of tokens and lse. */
+hdf_status hdf_sample_tokens(const float* logits, int64_t rows, int vocab, int64_t ld,
+                             float temperature, uint64_t seed, uint64_t stream_id, int32_t* tokens,
+                             float* lse, void* ws, size_t ws_bytes, hdf_stream_t stream);
+/* Workspace bytes of hdf_accept_sample (0 on invalid arguments). */
+size_t hdf_accept_sample_workspace(int n_seq, int K, int vocab);
+/* draft          int32, draft i of sequence s at draft[s*draft_stride + i] (drawn from
+ *                the draft distributions, e.g. hdf_sample_tokens on the LM head logits)
+ * draft_logits   fp32, the logits of draft i of sequence s at row s*draft_stride + i of
+ *                a matrix with row stride ld (the rows the drafts were drawn from)
+ * draft_lse      fp32 [same rows]: logsumexp(draft logits / temperature) (hdf_sample_tokens)
+ * target_logits  [n_seq][K+1][vocab] fp32: row i of sequence s holds the target's logits
+ *                for the token at draft position i (i = K: the token after the drafts)
+ * accept_len, next_anchor, commit_offsets, commit_tokens  as for hdf_accept; the
+ *                committed tokens of s are its accepted drafts followed by the drawn token
+ * With the LM head's logits of a block (row s*B + k is slot k): draft = tokens + 1,
+ * draft_logits = logits + vocab, draft_lse = lse + 1, draft_stride = B, ld = vocab,
+ * K = B - 1.
+ * ws, ws_bytes   at least hdf_accept_sample_workspace(n_seq, K, vocab) bytes, 256-byte
+ *                aligned; its contents on entry do not matter.
+ * Limits: n_seq >= 0, 0 <= K <= 1024, n_seq * (K + 1) <= 65535, 0 < temperature < inf. */
+hdf_status hdf_accept_sample(const int32_t* draft, int draft_stride, const float* draft_logits,
+                             const float* draft_lse, int64_t ld, const float* target_logits,
+                             int n_seq, int K, int vocab, float temperature, uint64_t seed,
+                             uint64_t stream_id, int32_t* accept_len, int32_t* next_anchor,
+                             int32_t* commit_offsets, int32_t* commit_tokens, void* ws,
+                             size_t ws_bytes, hdf_stream_t stream);
 
 #ifdef __cplusplus
 }

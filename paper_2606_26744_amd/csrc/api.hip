@@ -275,6 +275,72 @@ hdf_status hdf_fc_reduce(const void* H, const void* W_fc, const float* b_fc, int
   return ok();
 }
 
+size_t hdf_sample_workspace(int64_t rows, int vocab) {
+  if (rows < 0 || vocab < 1) return 0;
+  return (hdf::sample_parts_bytes(rows, vocab) + 255) / 256 * 256;
+}
+
+hdf_status hdf_sample_tokens(const float* logits, int64_t rows, int vocab, int64_t ld,
+                             float temperature, uint64_t seed, uint64_t stream_id, int32_t* tokens,
+                             float* lse, void* ws, size_t ws_bytes, hdf_stream_t stream) {
+  if (rows < 0 || vocab < 1) return fail(HDF_E_INVALID, "sample_tokens: rows=%lld vocab=%d",
+                                          static_cast<long long>(rows), vocab);
+  if (ld < vocab) return fail(HDF_E_INVALID, "sample_tokens: ld < vocab");
+  if (!(temperature > 0.f) || !(temperature < INFINITY))
+    return fail(HDF_E_INVALID, "sample_tokens: temperature must be positive and finite");
+  if (rows > 65535) return fail(HDF_E_UNSUPPORTED, "sample_tokens: more than 65535 rows");
+  if (rows == 0) return ok();
+  if (logits == nullptr || (tokens == nullptr && lse == nullptr))
+    return fail(HDF_E_INVALID, "sample_tokens: null pointer");
+  const size_t need = hdf_sample_workspace(rows, vocab);
+  if (ws == nullptr || ws_bytes < need)
+    return fail(HDF_E_WORKSPACE, "sample_tokens: workspace of %zu bytes needed, %zu given", need,
+                ws_bytes);
+  hipError_t e = hdf::launch_row_softmax(logits, rows, vocab, ld, 1.f / temperature,
+                                         tokens != nullptr, seed, stream_id, tokens, lse, ws,
+                                         reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "sample_tokens launch");
+  return ok();
+}
+
+size_t hdf_accept_sample_workspace(int n_seq, int K, int vocab) {
+  if (n_seq < 0 || K < 0 || vocab < 1) return 0;
+  return hdf::accept_sample_ws_bytes(n_seq, K, vocab);
+}
+
+hdf_status hdf_accept_sample(const int32_t* draft, int draft_stride, const float* draft_logits,
+                             const float* draft_lse, int64_t ld, const float* target_logits,
+                             int n_seq, int K, int vocab, float temperature, uint64_t seed,
+                             uint64_t stream_id, int32_t* accept_len, int32_t* next_anchor,
+                             int32_t* commit_offsets, int32_t* commit_tokens, void* ws,
+                             size_t ws_bytes, hdf_stream_t stream) {
+  if (n_seq < 0) return fail(HDF_E_INVALID, "accept_sample: n_seq < 0");
+  if (K < 0 || K > 1024) return fail(HDF_E_INVALID, "accept_sample: K=%d outside [0, 1024]", K);
+  if (vocab < 1) return fail(HDF_E_INVALID, "accept_sample: vocab < 1");
+  if (draft_stride < K) return fail(HDF_E_INVALID, "accept_sample: draft_stride < K");
+  if (K > 0 && ld < vocab) return fail(HDF_E_INVALID, "accept_sample: ld < vocab");
+  if (!(temperature > 0.f) || !(temperature < INFINITY))
+    return fail(HDF_E_INVALID, "accept_sample: temperature must be positive and finite");
+  if (n_seq > 65535 || int64_t(n_seq) * (K + 1) > 65535)
+    return fail(HDF_E_UNSUPPORTED, "accept_sample: more than 65535 target rows");
+  if (n_seq == 0) return ok();
+  if ((K > 0 && (draft == nullptr || draft_logits == nullptr || draft_lse == nullptr)) ||
+      target_logits == nullptr || accept_len == nullptr || next_anchor == nullptr)
+    return fail(HDF_E_INVALID, "accept_sample: null pointer");
+  const size_t need = hdf::accept_sample_ws_bytes(n_seq, K, vocab);
+  if (ws == nullptr || ws_bytes < need)
+    return fail(HDF_E_WORKSPACE, "accept_sample: workspace of %zu bytes needed, %zu given", need,
+                ws_bytes);
+  if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0)
+    return fail(HDF_E_INVALID, "accept_sample: workspace must be 256-byte aligned");
+  hipError_t e = hdf::launch_accept_sample(draft, draft_stride, draft_logits, draft_lse, ld,
+                                           target_logits, n_seq, K, vocab, 1.f / temperature, seed,
+                                           stream_id, accept_len, next_anchor, commit_offsets,
+                                           commit_tokens, ws, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "accept_sample launch");
+  return ok();
+}
+
 hdf_status hdf_accept(const int32_t* draft, int draft_stride, const int32_t* target, int n_seq,
                       int K, int32_t* accept_len, int32_t* next_anchor, int32_t* commit_offsets,
                       int32_t* commit_tokens, hdf_stream_t stream) {

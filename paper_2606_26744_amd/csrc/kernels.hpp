@@ -135,6 +135,22 @@ hipError_t launch_split_sum_store(bool bf16, const float* parts, int S, int64_t 
 hipError_t launch_silu_epilogue(bool bf16, const float* parts, int S, int64_t M, int F, void* act,
                                 hipStream_t s);
 
+// ---------------------------------------------------------------- sampling (sample.hip)
+// Workspace bytes of launch_row_softmax for `rows` rows of V columns.
+size_t sample_parts_bytes(int64_t rows, int V);
+// Per row of logits [rows][ld]: lse = logsumexp(logits * inv_t) and, with `sample`, a
+// token drawn from softmax(logits * inv_t) (Philox4x64-10 Gumbel noise); tokens/lse may
+// be NULL.
+hipError_t launch_row_softmax(const float* logits, int64_t rows, int V, int64_t ld, float inv_t,
+                              bool sample, uint64_t seed, uint64_t stream, int32_t* tokens,
+                              float* lse, void* part_ws, hipStream_t s);
+size_t accept_sample_ws_bytes(int n_seq, int K, int V);
+hipError_t launch_accept_sample(const int32_t* draft, int draft_stride, const float* draft_logits,
+                                const float* draft_lse, int64_t ld, const float* target_logits,
+                                int n_seq, int K, int V, float inv_t, uint64_t seed,
+                                uint64_t stream, int32_t* acc, int32_t* anchor, int32_t* offs,
+                                int32_t* toks, void* ws, hipStream_t s);
+
 // ---------------------------------------------------------------- attention (attention.hip)
 struct AttnArgs {
   const void* q;             // [n_seq][nh][B][hd]

@@ -25,7 +25,9 @@ EXPORTS = ("hdf_last_error", "hdf_version", "hdf_hc_reduce", "hdf_rope_table",
            "hdf_packed_weight_bytes", "hdf_pack_weight",
            "hdf_kv_cache_bytes", "hdf_draft_block_workspace", "hdf_draft_block",
            "hdf_draft_block_paged", "hdf_fc_reduce_workspace", "hdf_fc_reduce",
-           "hdf_lm_head_workspace", "hdf_lm_head_argmax", "hdf_accept")
+           "hdf_lm_head_workspace", "hdf_lm_head_argmax", "hdf_accept",
+           "hdf_sample_workspace", "hdf_sample_tokens", "hdf_accept_sample_workspace",
+           "hdf_accept_sample")
 
 
 class HdfError(RuntimeError):
@@ -99,6 +101,16 @@ def lib() -> ctypes.CDLL:
     L.hdf_lm_head_argmax.argtypes = [_P, _P, _I64, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]
     L.hdf_accept.restype = _I
     L.hdf_accept.argtypes = [_P, _I, _P, _I, _I, _P, _P, _P, _P, _P]
+    _U64 = ctypes.c_uint64
+    L.hdf_sample_workspace.restype = _SZ
+    L.hdf_sample_workspace.argtypes = [_I64, _I]
+    L.hdf_sample_tokens.restype = _I
+    L.hdf_sample_tokens.argtypes = [_P, _I64, _I, _I64, _F, _U64, _U64, _P, _P, _P, _SZ, _P]
+    L.hdf_accept_sample_workspace.restype = _SZ
+    L.hdf_accept_sample_workspace.argtypes = [_I, _I, _I]
+    L.hdf_accept_sample.restype = _I
+    L.hdf_accept_sample.argtypes = [_P, _I, _P, _P, _I64, _P, _I, _I, _I, _F, _U64, _U64, _P, _P,
+                                    _P, _P, _P, _SZ, _P]
     _lib = L
     return L
 
@@ -191,6 +203,53 @@ def accept(draft: torch.Tensor, target: torch.Tensor, *, K: Optional[int] = None
         raise ValueError("libhdf takes device tensors")
     _check(lib().hdf_accept(_ptr(draft), draft_stride, _ptr(target), n_seq, K, _ptr(acc),
                             _ptr(anc), _ptr(offs), _ptr(toks), _stream(stream)))
+    return acc, anc, offs, toks
+
+
+# ----------------------------------------------------------------------------- sampling
+
+def sample_tokens(logits: torch.Tensor, *, temperature: float = 1.0, seed: int = 0,
+                  stream_id: int = 0, want_tokens: bool = True, ws=None, out=None, stream=None):
+    """hdf_sample_tokens: logits [rows, vocab] fp32 -> (tokens [rows] int32 or None,
+    lse [rows] fp32)."""
+    rows, V = logits.shape
+    dev = logits.device
+    if out is None:
+        tok = torch.empty(rows, dtype=torch.int32, device=dev) if want_tokens else None
+        lse = torch.empty(rows, dtype=torch.float32, device=dev)
+    else:
+        tok, lse = out
+    need = int(lib().hdf_sample_workspace(rows, V))
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    if logits.dtype != torch.float32 or logits.stride(1) != 1:
+        raise ValueError("logits must be fp32 with unit column stride")
+    _check(lib().hdf_sample_tokens(_ptr(logits), rows, V, logits.stride(0), float(temperature),
+                                   int(seed), int(stream_id), _ptr(tok), _ptr(lse), _ptr(ws),
+                                   ws.numel(), _stream(stream)))
+    return tok, lse
+
+
+def accept_sample(draft: torch.Tensor, draft_logits: torch.Tensor, draft_lse: torch.Tensor,
+                  target_logits: torch.Tensor, *, K: int, draft_stride: int, ld: int,
+                  temperature: float = 1.0, seed: int = 0, stream_id: int = 0, ws=None,
+                  stream=None):
+    """hdf_accept_sample.  draft / draft_logits / draft_lse are base pointers (tensors
+    or views) addressed as in hdf.h; target_logits [n_seq, K+1, vocab] fp32."""
+    n_seq, _, V = target_logits.shape
+    dev = target_logits.device
+    acc = torch.empty(n_seq, dtype=torch.int32, device=dev)
+    anc = torch.empty(n_seq, dtype=torch.int32, device=dev)
+    offs = torch.empty(n_seq + 1, dtype=torch.int32, device=dev)
+    toks = torch.empty(max(1, n_seq * (K + 1)), dtype=torch.int32, device=dev)
+    need = int(lib().hdf_accept_sample_workspace(n_seq, K, V))
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _dev(target_logits, acc, ws)
+    _check(lib().hdf_accept_sample(_ptr(draft), draft_stride, _ptr(draft_logits), _ptr(draft_lse),
+                                   ld, _ptr(target_logits), n_seq, K, V, float(temperature),
+                                   int(seed), int(stream_id), _ptr(acc), _ptr(anc), _ptr(offs),
+                                   _ptr(toks), _ptr(ws), ws.numel(), _stream(stream)))
     return acc, anc, offs, toks
 
 
