@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--decode", type=int, default=0, metavar="R",
                     help="also time R chained rounds of the paged decode loop (8 sequences "
                          "from 2048 positions, n+1 committed positions appended per round)")
+    ap.add_argument("--temperature", type=float, default=0.0, metavar="T",
+                    help="also time the step at temperature T > 0 (draws from softmax(z / T) and "
+                         "speculative-sampling verification against synthetic target logits)")
     ap.add_argument("--fc-reducer", action="store_true",
                     help="also time the generic fc reducer beside the gated one (warm-step "
                          "rows and the reducer-stress shape)")
@@ -224,6 +227,41 @@ def decode_leg(torch, synth, hdf, rounds, warmup):
            "mean_accept_len": round(committed / (rounds * n_seq) - 1, 3),
            "context_end": [int(x) for x in dec.ctx], "pages_used": n_pages - dec.pool.free}
     del dec, h, w, red
+    torch.cuda.empty_cache()
+    return res
+
+
+def sampled_leg(torch, synth, hdf, wl, h, bufs, args, T, steps, warmup):
+    """The full-size step at temperature T: the same step with the LM head's logits kept,
+    a draw for every slot and speculative-sampling verification.  The target's logits are
+    synthetic: the draft logits of an untimed step plus N(0, 0.5) noise."""
+    from paper_2606_26744_amd.step import SampledStepBuffers, drafter_step_sampled
+    n_seq, B, V = wl.n_seq, wl.block, h.V
+    sb = SampledStepBuffers(h, n_seq, B)
+    kw = {k: v for k, v in args.items()}
+    tgt = torch.zeros((n_seq, B, V), dtype=torch.float32, device="cuda")
+    out = drafter_step_sampled(h, bufs, sb, target_logits=tgt, temperature=T, **kw)
+    g = torch.Generator(device="cuda").manual_seed(wl.seed)
+    lg = out["logits"].view(n_seq, B, V)
+    tgt[:, :B - 1] = lg[:, 1:] + 0.5 * torch.randn((n_seq, B - 1, V), generator=g, device="cuda")
+    tgt[:, B - 1] = lg[:, 0]
+    for r in range(warmup):
+        drafter_step_sampled(h, bufs, sb, target_logits=tgt, temperature=T, round_id=r, **kw)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    accs = []
+    torch.cuda.synchronize()
+    e0.record()
+    for r in range(steps):
+        out = drafter_step_sampled(h, bufs, sb, target_logits=tgt, temperature=T,
+                                   round_id=warmup + r, **kw)
+        accs.append(out["accept_len"])
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    acc = torch.stack(accs).float()
+    res = {"temperature": T, "ms_per_step": round(ms, 4), "blocks_per_s": round(n_seq / (ms * 1e-3), 1),
+           "steps": steps, "mean_accept_len": round(float(acc.mean()), 3)}
+    del sb, tgt
     torch.cuda.empty_cache()
     return res
 
@@ -469,6 +507,9 @@ def main():
         del x, y
     if not a.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(torch, synth, wl, h, w, red, args, offs)
+    if a.temperature > 0:
+        res["sampled_step"] = sampled_leg(torch, synth, hdf, wl, h, bufs, args, a.temperature,
+                                          a.steps, 3)
     if a.fc_reducer:
         res["fc_reducer"] = fc_reducer_leg(torch, synth, hdf)
     if a.blas_ref:

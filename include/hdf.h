@@ -310,8 +310,9 @@ hdf_status hdf_accept(const int32_t* draft, int draft_stride, const int32_t* tar
  *     at the first rejection n the next token is drawn from max(0, p_n - q_n)
  *     renormalised; after K acceptances it is drawn from p_K (the bonus token).
  * Random numbers come from Philox4x64-10 (Salmon et al., SC'11) with key
- * (seed, stream_id) and counter (row, v/4, purpose, 0); word v%4 of the block gives
- * u = (its top 24 bits + 1/2) / 2^24.  Purpose 0: the noise of hdf_sample_tokens
+ * (seed, stream_id) and counter (row, v/8, purpose, 0); word (v%8)/2 of the block gives
+ * two uniforms, from its high 32 bits for even v and its low 32 bits for odd v:
+ * u = (top 24 bits of the half + 1/2) / 2^24.  Purpose 0: the noise of hdf_sample_tokens
  * (row = logits row, v = token); 1: the acceptance uniform of draft i of sequence s
  * (row = s, v = i); 2: the noise of the final draw of sequence s (row = s, v = token).
  * Draws from softmax(x) are argmax_v (x_v - log(-log u_v)) (Gumbel-max).

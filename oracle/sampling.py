@@ -13,8 +13,9 @@ max(0, p_n - q_n) renormalised; when all K drafts are accepted it is drawn from 
 Random numbers (so that the GPU path and this oracle draw the same ones): the
 counter-based generator Philox4x64-10 (Salmon, Moraes, Dror, Shaw, "Parallel random
 numbers: as easy as 1, 2, 3", SC'11) with key (seed, stream) and counter
-(row, v // 4, purpose, 0); word v % 4 of the output block gives the uniform
-u = (top 24 bits + 1/2) / 2^24, in (0, 1).  Purposes: 0 = Gumbel noise of draft
+(row, v // 8, purpose, 0); of the block's four 64-bit words, word (v % 8) // 2 gives
+two uniforms, one from each 32-bit half (the high half for even v, the low half for
+odd v): u = (top 24 bits of the half + 1/2) / 2^24, in (0, 1).  Purposes: 0 = Gumbel noise of draft
 sampling (row = logits row, v = vocabulary index), 1 = acceptance uniforms
 (row = sequence, v = slot), 2 = Gumbel noise of the residual or bonus sample
 (row = sequence, v = vocabulary index).  A sample from softmax(s) is
@@ -65,12 +66,14 @@ def uniforms(seed: int, stream: int, rows, vs, purpose: int) -> np.ndarray:
     """u for every (row, v) pair (broadcast shapes), float64 in (0, 1)."""
     rows, vs = np.broadcast_arrays(np.asarray(rows, dtype=np.uint64),
                                    np.asarray(vs, dtype=np.uint64))
-    ctr = np.stack([rows, vs >> np.uint64(2), np.full(rows.shape, purpose, dtype=np.uint64),
+    ctr = np.stack([rows, vs >> np.uint64(3), np.full(rows.shape, purpose, dtype=np.uint64),
                     np.zeros(rows.shape, dtype=np.uint64)], axis=-1)
     key = np.broadcast_to(np.array([seed, stream], dtype=np.uint64), rows.shape + (2,))
     out = philox4x64_10(ctr, key)
-    word = np.take_along_axis(out, (vs & np.uint64(3)).astype(np.int64)[..., None], axis=-1)[..., 0]
-    return ((word >> np.uint64(40)).astype(np.float64) + 0.5) / float(1 << 24)
+    j = ((vs & np.uint64(7)) >> np.uint64(1)).astype(np.int64)
+    word = np.take_along_axis(out, j[..., None], axis=-1)[..., 0]
+    half = np.where((vs & np.uint64(1)) == 0, word >> np.uint64(32), word & _LO32)
+    return ((half >> np.uint64(8)).astype(np.float64) + 0.5) / float(1 << 24)
 
 
 def gumbel(u: np.ndarray) -> np.ndarray:

@@ -5,7 +5,8 @@
 // max(0, p - q) renormalised, after K acceptances draw the bonus from p_K).
 //
 // Random numbers: Philox4x64-10 (Salmon et al., SC'11), key (seed, stream), counter
-// (row, v/4, purpose, 0), word v%4 -> u = (top 24 bits + 1/2) * 2^-24.  A draw from
+// (row, v/8, purpose, 0); word (v%8)/2 of the block gives two uniforms, from its high
+// 32 bits for even v and its low 32 bits for odd v: u = (top 24 bits + 1/2) * 2^-24.  A draw from
 // softmax(s) is argmax_v (s_v - log(-log u_v)) (Gumbel-max), so no probability vector
 // is ever materialised: a pass over the logits keeps a running log-sum-exp and the
 // best perturbed score.
@@ -36,14 +37,19 @@ __device__ __forceinline__ void philox4x64_10(uint64_t c[4], uint64_t k0, uint64
   }
 }
 
-// Uniforms of the four vocabulary entries 4*g .. 4*g+3 of one row.
-__device__ __forceinline__ void uniforms4(uint64_t seed, uint64_t stream, uint64_t row, uint64_t g,
-                                          int purpose, float u[4]) {
+// Uniforms of the eight entries 8*g .. 8*g+7 of one row.
+__device__ __forceinline__ void uniforms8(uint64_t seed, uint64_t stream, uint64_t row, uint64_t g,
+                                          int purpose, float u[8]) {
   uint64_t c[4] = {row, g, uint64_t(purpose), 0ull};
   philox4x64_10(c, seed, stream);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) u[j] = (float(uint32_t(c[j] >> 40)) + 0.5f) * 5.9604644775390625e-8f;
+  for (int j = 0; j < 4; ++j) {
+    u[2 * j] = (float(uint32_t(c[j] >> 40)) + 0.5f) * 5.9604644775390625e-8f;
+    u[2 * j + 1] = (float(uint32_t(c[j] & 0xFFFFFFFFull) >> 8) + 0.5f) * 5.9604644775390625e-8f;
+  }
 }
+
+constexpr int kGroupsPerPass = 4;   // 8-entry groups each thread loads before computing
 
 __device__ __forceinline__ float gumbel(float u) { return -logf(-logf(u)); }
 
@@ -113,9 +119,11 @@ __device__ RowState block_merge(RowState st, RowState* sh) {
   return t;
 }
 
-// Pass over logits row `row`, columns [c0, c1) (c0 % 4 == 0): partial log-sum-exp of
+// Pass over logits row `row`, columns [c0, c1) (c0 % 8 == 0): partial log-sum-exp of
 // logits * inv_t and, with SAMPLE, the Gumbel-max draw.  Partial j of the row goes to
-// part[row * n_parts + j].
+// part[row * n_parts + j].  Each thread loads kGroupsPerPass groups of eight logits
+// (two 16-byte loads each when the row is 16-byte aligned) before it computes, so that
+// the loads of a pass are in flight together.
 template <bool SAMPLE>
 __global__ void __launch_bounds__(kSampleThreads)
 row_pass_kernel(const float* __restrict__ logits, int64_t ld, int V, int n_parts, int chunk,
@@ -125,17 +133,37 @@ row_pass_kernel(const float* __restrict__ logits, int64_t ld, int V, int n_parts
   const int j = blockIdx.y;
   const int c0 = j * chunk, c1 = min(V, c0 + chunk);
   const float* z = logits + row * ld;
+  const bool vec = (reinterpret_cast<uintptr_t>(z) & 15u) == 0;
   RowState st{-INFINITY, 0.f, -INFINITY, 0x7FFFFFFF};
-  for (int g = c0 / 4 + threadIdx.x; 4 * g < c1; g += kSampleThreads) {
-    float u[4];
-    if constexpr (SAMPLE) uniforms4(seed, stream, uint64_t(row), uint64_t(g), kPurposeDraft, u);
+  for (int g0 = c0 / 8 + threadIdx.x; 8 * g0 < c1; g0 += kSampleThreads * kGroupsPerPass) {
+    float x[kGroupsPerPass][8];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int v = 4 * g + k;
-      if (v < c1) {
-        const float x = z[v] * inv_t;
-        lse_add(st, x);
-        if constexpr (SAMPLE) best_add(st, x + gumbel(u[k]), v);
+    for (int q = 0; q < kGroupsPerPass; ++q) {
+      const int v0 = 8 * (g0 + q * kSampleThreads);
+      if (vec && v0 + 8 <= c1) {
+        const float4 a = *reinterpret_cast<const float4*>(z + v0);
+        const float4 b = *reinterpret_cast<const float4*>(z + v0 + 4);
+        x[q][0] = a.x; x[q][1] = a.y; x[q][2] = a.z; x[q][3] = a.w;
+        x[q][4] = b.x; x[q][5] = b.y; x[q][6] = b.z; x[q][7] = b.w;
+      } else {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) x[q][k] = (v0 + k < c1) ? z[v0 + k] : 0.f;
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kGroupsPerPass; ++q) {
+      const int g = g0 + q * kSampleThreads;
+      if (8 * g >= c1) continue;
+      float u[8];
+      if constexpr (SAMPLE) uniforms8(seed, stream, uint64_t(row), uint64_t(g), kPurposeDraft, u);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int v = 8 * g + k;
+        if (v < c1) {
+          const float xs = x[q][k] * inv_t;
+          lse_add(st, xs);
+          if constexpr (SAMPLE) best_add(st, xs + gumbel(u[k]), v);
+        }
       }
     }
   }
@@ -155,11 +183,12 @@ __global__ void row_finish_kernel(const RowState* __restrict__ part, int64_t row
 }
 
 static void row_split(int64_t rows, int V, int& n_parts, int& chunk) {
-  // Enough workgroups for two per CU, each at least 4096 columns wide.
-  const int64_t want = (2 * int64_t(device_cu_count()) + rows - 1) / (rows > 0 ? rows : 1);
-  const int max_parts = (V + 4095) / 4096;
+  // Enough workgroups for four per CU, each at least 2048 columns wide; chunks are
+  // whole 8-entry groups.
+  const int64_t want = (4 * int64_t(device_cu_count()) + rows - 1) / (rows > 0 ? rows : 1);
+  const int max_parts = (V + 2047) / 2048;
   n_parts = int(want < 1 ? 1 : (want > max_parts ? max_parts : want));
-  chunk = ((V + n_parts - 1) / n_parts + 3) / 4 * 4;
+  chunk = ((V + n_parts - 1) / n_parts + 7) / 8 * 8;
   n_parts = (V + chunk - 1) / chunk;
 }
 
@@ -212,9 +241,9 @@ accept_decide_kernel(const int32_t* __restrict__ draft, int draft_stride,
       const float q = __expf(draft_logits[dr * ld + x] * inv_t - draft_lse[dr]);
       const int64_t tr = int64_t(s) * (K + 1) + i;
       const float p = __expf(target_logits[tr * V + x] * inv_t - target_lse[tr]);
-      float u[4];
-      uniforms4(seed, stream, uint64_t(s), uint64_t(i >> 2), kPurposeAccept, u);
-      reject = !(u[i & 3] * q < p);
+      float u[8];
+      uniforms8(seed, stream, uint64_t(s), uint64_t(i >> 3), kPurposeAccept, u);
+      reject = !(u[i & 7] * q < p);
     }
     const unsigned long long m = __ballot(reject);
     if (m != 0ull) {
@@ -255,12 +284,12 @@ accept_draw_kernel(const float* __restrict__ draft_logits, const float* __restri
   const int c0 = j * chunk, c1 = min(V, c0 + chunk);
   RowState a{-INFINITY, 0.f, -INFINITY, 0x7FFFFFFF};   // residual / bonus
   RowState b{-INFINITY, 0.f, -INFINITY, 0x7FFFFFFF};   // log p_n fallback
-  for (int g = c0 / 4 + threadIdx.x; 4 * g < c1; g += kSampleThreads) {
-    float u[4];
-    uniforms4(seed, stream, uint64_t(s), uint64_t(g), kPurposeResample, u);
+  for (int g = c0 / 8 + threadIdx.x; 8 * g < c1; g += kSampleThreads) {
+    float u[8];
+    uniforms8(seed, stream, uint64_t(s), uint64_t(g), kPurposeResample, u);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int v = 4 * g + k;
+    for (int k = 0; k < 8; ++k) {
+      const int v = 8 * g + k;
       if (v < c1) {
         const float gm = gumbel(u[k]);
         const float lp = zt[v] * inv_t - lt;

@@ -289,9 +289,10 @@ def lm_head_workspace(M: int, vocab: int) -> int:
 
 def lm_head_argmax(hidden: torch.Tensor, w_lm: PackedWeight, *, want_logits: bool = False,
                    want_max: bool = True, ws: Optional[torch.Tensor] = None, out=None,
-                   stream=None):
+                   logits_out: Optional[torch.Tensor] = None, stream=None):
     """hdf_lm_head_argmax: hidden [M, d], packed w_lm [V, d] -> (argmax int32 [M], max fp32
-    [M], logits fp32 [M, V] or None)."""
+    [M], logits fp32 [M, V] or None).  logits_out: a preallocated [M, V] fp32 tensor for
+    the logits (implies want_logits)."""
     if not isinstance(w_lm, PackedWeight):
         raise TypeError("w_lm must be packed with pack_weight()")
     M, d = hidden.shape
@@ -304,7 +305,12 @@ def lm_head_argmax(hidden: torch.Tensor, w_lm: PackedWeight, *, want_logits: boo
         mx = torch.empty(M, dtype=torch.float32, device=dev) if want_max else None
     else:
         am, mx = out
-    lg = torch.empty((M, V), dtype=torch.float32, device=dev) if want_logits else None
+    if logits_out is not None:
+        if logits_out.shape != (M, V) or logits_out.dtype != torch.float32:
+            raise ValueError("logits_out must be a [M, V] fp32 tensor")
+        lg = logits_out
+    else:
+        lg = torch.empty((M, V), dtype=torch.float32, device=dev) if want_logits else None
     need = lm_head_workspace(M, V)
     if ws is None or ws.numel() < need:
         ws = torch.zeros(max(need, 1), dtype=torch.uint8, device=dev)   # zero before first use

@@ -17,6 +17,22 @@ import torch
 from . import hdf
 
 
+class SampledStepBuffers:
+    """Extra device buffers of a temperature-sampled step: fp32 logits [n_seq*B][V],
+    drawn tokens, log-sum-exps and the two sampling workspaces."""
+
+    def __init__(self, handle: hdf.DrafterHandle, n_seq: int, B: int, device="cuda"):
+        M, V = n_seq * B, handle.V
+        self.logits = torch.empty((M, V), dtype=torch.float32, device=device)
+        self.tokens = torch.empty(M, dtype=torch.int32, device=device)
+        self.lse = torch.empty(M, dtype=torch.float32, device=device)
+        self.sample_ws = torch.empty(max(int(hdf.lib().hdf_sample_workspace(M, V)), 1),
+                                     dtype=torch.uint8, device=device)
+        self.accept_ws = torch.empty(
+            max(int(hdf.lib().hdf_accept_sample_workspace(n_seq, B - 1, V)), 1),
+            dtype=torch.uint8, device=device)
+
+
 class StepBuffers:
     """Device buffers of one step, reused across steps (nothing is allocated per call)."""
 
@@ -70,3 +86,35 @@ def drafter_step(handle: hdf.DrafterHandle, bufs: StepBuffers, *, H_new: torch.T
         out.update(accept_len=acc, next_anchor=anc, commit_offsets=offs, commit_tokens=toks)
     mark(4)
     return out
+
+
+def drafter_step_sampled(handle: hdf.DrafterHandle, bufs: StepBuffers, sbufs: SampledStepBuffers,
+                         *, H_new: torch.Tensor, W_g: torch.Tensor, b_g: torch.Tensor,
+                         new_offsets: torch.Tensor, ctx_len: torch.Tensor, max_ctx: int,
+                         kv_offsets: torch.Tensor, kv_k: torch.Tensor, kv_vt: torch.Tensor,
+                         tokens: torch.Tensor, target_logits: torch.Tensor,
+                         temperature: float = 1.0, seed: int = 0, round_id: int = 0,
+                         reduce_kw: Optional[dict] = None, stream=None):
+    """The step at temperature T: reduce -> draft block -> LM head (logits kept) ->
+    draws of every slot from softmax(logits / T) -> speculative-sampling verification
+    against target_logits [n_seq, B, V] (row i: the target's logits for draft slot i+1;
+    the last row for the token after the drafts).  round_id selects the Philox stream,
+    so that every round draws fresh numbers."""
+    kw = dict(reduce_kw or {})
+    kw.setdefault("eps", handle.eps)
+    hdf.hc_reduce(H_new, W_g, b_g, Y=bufs.Y, stream=stream, **kw)
+    handle.draft_block(ctx_len=ctx_len, max_ctx=max_ctx, y_new=bufs.Y, new_offsets=new_offsets,
+                       kv_offsets=kv_offsets, kv_k=kv_k, kv_vt=kv_vt, tokens=tokens,
+                       hidden=bufs.hidden, ws=bufs.ws, stream=stream)
+    hdf.lm_head_argmax(bufs.hidden, handle.w_lm, ws=bufs.lm_ws, out=(bufs.argmax, bufs.max_logit),
+                       logits_out=sbufs.logits, stream=stream)
+    hdf.sample_tokens(sbufs.logits, temperature=temperature, seed=seed, stream_id=2 * round_id,
+                      ws=sbufs.sample_ws, out=(sbufs.tokens, sbufs.lse), stream=stream)
+    n_seq, B = tokens.shape
+    V = handle.V
+    acc, anc, offs, toks = hdf.accept_sample(
+        sbufs.tokens[1:], sbufs.logits[1:], sbufs.lse[1:], target_logits, K=B - 1,
+        draft_stride=B, ld=V, temperature=temperature, seed=seed, stream_id=2 * round_id + 1,
+        ws=sbufs.accept_ws, stream=stream)
+    return {"hidden": bufs.hidden, "logits": sbufs.logits, "tokens": sbufs.tokens,
+            "accept_len": acc, "next_anchor": anc, "commit_offsets": offs, "commit_tokens": toks}

@@ -127,3 +127,43 @@ def test_ragged_step_subset():
     ctx = wl.ctx_lens[:6]
     _step_case(wl, ctx, [16] * 6, seqs=[int(np.argmin(ctx)), int(np.argmax(ctx))], sub=2)
     torch.cuda.empty_cache()
+
+
+def test_sampled_step_wiring():
+    """The temperature-sampled step (drafter_step_sampled): its draws come from its own
+    logits and its verification equals the oracle's on the same logits, tokens and
+    target logits (checks the slot offsets and strides of the sampled path)."""
+    from oracle.sampling import accept_sample as ref_accept_sample, sample_tokens as ref_sample
+    from paper_2606_26744_amd.step import SampledStepBuffers, drafter_step_sampled
+    wl = synth.small_bf16()
+    ctx, new = [512] * 4, [16] * 4
+    n_new = sum(new)
+    red = synth.reducer_inputs(wl, n_new, device="cuda", sub=5)
+    case = DraftCase(wl, ctx, new, random_norms=False, sub=5,
+                     y_from=torch.empty((n_new, wl.d), dtype=red["H"].dtype, device="cuda"))
+    n_seq, B, V = len(ctx), case.B, wl.drafter.vocab
+    bufs = StepBuffers(case.h, n_seq, B, n_new, case.max_ctx, wl.m)
+    sb = SampledStepBuffers(case.h, n_seq, B)
+    g = torch.Generator(device="cuda").manual_seed(1)
+    tgt = 2.0 * torch.randn((n_seq, B, V), generator=g, device="cuda")
+    kw = dict(H_new=red["H"], W_g=red["W_g"], b_g=red["b_g"], new_offsets=case.new_offsets,
+              ctx_len=case.ctx_len, max_ctx=case.max_ctx, kv_offsets=case.kv_offsets,
+              kv_k=case.kv_k, kv_vt=case.kv_vt, tokens=case.tokens)
+    out = drafter_step_sampled(case.h, bufs, sb, target_logits=tgt, temperature=1.0, seed=7,
+                               round_id=3, **kw)
+    torch.cuda.synchronize()
+    lg = out["logits"].cpu().numpy()
+    tok = out["tokens"].cpu().numpy()
+    r_tok, _, margin = ref_sample(lg, 1.0, 7, 6)                  # stream 2 * round_id
+    ok = margin >= 1e-3
+    assert ok.mean() > 0.9 and np.array_equal(tok[ok], r_tok[ok])
+    drafts = tok.reshape(n_seq, B)[:, 1:]
+    dl = lg.reshape(n_seq, B, V)[:, 1:]
+    r_acc, r_anc, _, _, dmarg, smarg = ref_accept_sample(drafts, dl, tgt.cpu().numpy(), 1.0, 7, 7)
+    acc = out["accept_len"].cpu().numpy()
+    anc = out["next_anchor"].cpu().numpy()
+    good = dmarg >= 1e-4
+    assert good.mean() > 0.5
+    assert np.array_equal(acc[good], r_acc[good])
+    good &= smarg >= 1e-3
+    assert np.array_equal(anc[good], r_anc[good])
