@@ -351,6 +351,34 @@ hdf_status hdf_accept_sample(const int32_t* draft, int draft_stride, const float
                              int32_t* commit_offsets, int32_t* commit_tokens, void* ws,
                              size_t ws_bytes, hdf_stream_t stream);
 
+/* ------------------------------------------------------------------------------
+ * 6. LM-head KL distillation forward (Sec. 2.4, a training-side objective).
+ *
+ * For block s anchored at position a, draft position k = 1..P (the token at a+k) is
+ * supervised by the teacher t_k = LMHead(h_{a+k-1}), h the mean of the target's m
+ * residual paths at that position and LMHead(h) = (RMSNorm(h) * gamma) W_lm^T:
+ *     kl[s][k-1] = KL(softmax(t_k / T) || softmax(z_k / T)),  z_k the draft logits of slot k
+ *     ce[s][k-1] = -log softmax(z_k)[labels[s][k-1]]          (k = 1..B-1)
+ *     loss = { L_KL = T^2/P * mean_s sum_k kl[s][k-1],  L_CE = mean ce,  L_CE + alpha L_KL }
+ * The pooled, normed teacher state is rounded to `dtype` before the projection.
+ * ----------------------------------------------------------------------------*/
+size_t hdf_kl_forward_workspace(int n_seq, int B, int P, int d, int vocab, hdf_dtype dtype);
+/* H_pos           [n_seq][P][m][d] dtype: target residual paths at positions a .. a+P-1
+ * gamma           [d] fp32 or NULL (ones); eps > 0
+ * W_lm            [vocab][d] dtype, packed (hdf_pack_weight)
+ * student_logits  fp32, slot k of block s at row s*B + k, row stride ld (the LM head's
+ *                 logits of the drafted blocks)
+ * labels          [n_seq][B-1] int32 ground-truth tokens of slots 1..B-1, or NULL (no CE)
+ * kl              [n_seq][P] fp32 (out); ce [n_seq][B-1] fp32 (out, may be NULL);
+ * loss            [3] fp32 (out, may be NULL): L_KL, L_CE (0 without labels), L
+ * Limits: 1 <= m <= 8; 2 <= B <= 64; 1 <= P <= B-1; d % 64 == 0, d <= 8192;
+ *         n_seq * B <= 65535; 0 < temperature < inf. */
+hdf_status hdf_kl_forward(const void* H_pos, int m, const float* gamma, float eps, const void* W_lm,
+                          int d, int vocab, hdf_dtype dtype, const float* student_logits,
+                          int64_t ld, int B, const int32_t* labels, int n_seq, int P,
+                          float temperature, float alpha, float* kl, float* ce, float* loss,
+                          void* ws, size_t ws_bytes, hdf_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -341,6 +341,47 @@ hdf_status hdf_accept_sample(const int32_t* draft, int draft_stride, const float
   return ok();
 }
 
+size_t hdf_kl_forward_workspace(int n_seq, int B, int P, int d, int vocab, hdf_dtype dtype) {
+  if (n_seq < 0 || B < 2 || P < 1 || P > B - 1 || d < 64 || vocab < 1 ||
+      (dtype != HDF_F32 && dtype != HDF_BF16))
+    return 0;
+  return hdf::kl_ws_bytes(n_seq, B, P, d, vocab, dtype == HDF_BF16);
+}
+
+hdf_status hdf_kl_forward(const void* H_pos, int m, const float* gamma, float eps, const void* W_lm,
+                          int d, int vocab, hdf_dtype dtype, const float* student_logits,
+                          int64_t ld, int B, const int32_t* labels, int n_seq, int P,
+                          float temperature, float alpha, float* kl, float* ce, float* loss,
+                          void* ws, size_t ws_bytes, hdf_stream_t stream) {
+  if (dtype != HDF_F32 && dtype != HDF_BF16) return fail(HDF_E_INVALID, "kl_forward: bad dtype");
+  if (n_seq < 0) return fail(HDF_E_INVALID, "kl_forward: n_seq < 0");
+  if (m < 1 || m > 8) return fail(HDF_E_INVALID, "kl_forward: m=%d outside [1, 8]", m);
+  if (B < 2 || B > 64) return fail(HDF_E_INVALID, "kl_forward: B=%d outside [2, 64]", B);
+  if (P < 1 || P > B - 1) return fail(HDF_E_INVALID, "kl_forward: P=%d outside [1, B-1]", P);
+  if (d % 64 != 0 || d < 64 || d > 8192)
+    return fail(HDF_E_INVALID, "kl_forward: d=%d must be a multiple of 64 up to 8192", d);
+  if (vocab < 1 || ld < vocab) return fail(HDF_E_INVALID, "kl_forward: vocab/ld");
+  if (!(eps > 0.f)) return fail(HDF_E_INVALID, "kl_forward: eps must be > 0");
+  if (!(temperature > 0.f) || !(temperature < INFINITY))
+    return fail(HDF_E_INVALID, "kl_forward: temperature must be positive and finite");
+  if (int64_t(n_seq) * B > 65535)
+    return fail(HDF_E_UNSUPPORTED, "kl_forward: more than 65535 draft rows");
+  if (n_seq == 0) return ok();
+  if (H_pos == nullptr || W_lm == nullptr || student_logits == nullptr || kl == nullptr)
+    return fail(HDF_E_INVALID, "kl_forward: null pointer");
+  const size_t need = hdf::kl_ws_bytes(n_seq, B, P, d, vocab, dtype == HDF_BF16);
+  if (ws == nullptr || ws_bytes < need)
+    return fail(HDF_E_WORKSPACE, "kl_forward: workspace of %zu bytes needed, %zu given", need,
+                ws_bytes);
+  if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0)
+    return fail(HDF_E_INVALID, "kl_forward: workspace must be 256-byte aligned");
+  hipError_t e = hdf::launch_kl_forward(dtype == HDF_BF16, H_pos, m, gamma, eps, W_lm, d, vocab,
+                                        student_logits, ld, B, labels, n_seq, P, temperature, alpha,
+                                        kl, ce, loss, ws, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "kl_forward launch");
+  return ok();
+}
+
 hdf_status hdf_accept(const int32_t* draft, int draft_stride, const int32_t* target, int n_seq,
                       int K, int32_t* accept_len, int32_t* next_anchor, int32_t* commit_offsets,
                       int32_t* commit_tokens, hdf_stream_t stream) {

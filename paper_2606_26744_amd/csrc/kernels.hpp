@@ -151,6 +151,13 @@ hipError_t launch_accept_sample(const int32_t* draft, int draft_stride, const fl
                                 uint64_t stream, int32_t* acc, int32_t* anchor, int32_t* offs,
                                 int32_t* toks, void* ws, hipStream_t s);
 
+// ---------------------------------------------------------------- KL forward (kl.hip)
+size_t kl_ws_bytes(int n_seq, int B, int P, int d, int V, bool bf16);
+hipError_t launch_kl_forward(bool bf16, const void* H_pos, int m, const float* gamma, float eps,
+                             const void* W_lm, int d, int V, const float* zl, int64_t ld, int B,
+                             const int32_t* labels, int n_seq, int P, float T, float alpha,
+                             float* kl, float* ce, float* loss, void* ws, hipStream_t s);
+
 // ---------------------------------------------------------------- attention (attention.hip)
 struct AttnArgs {
   const void* q;             // [n_seq][nh][B][hd]

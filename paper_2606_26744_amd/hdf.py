@@ -27,7 +27,7 @@ EXPORTS = ("hdf_last_error", "hdf_version", "hdf_hc_reduce", "hdf_rope_table",
            "hdf_draft_block_paged", "hdf_fc_reduce_workspace", "hdf_fc_reduce",
            "hdf_lm_head_workspace", "hdf_lm_head_argmax", "hdf_accept",
            "hdf_sample_workspace", "hdf_sample_tokens", "hdf_accept_sample_workspace",
-           "hdf_accept_sample")
+           "hdf_accept_sample", "hdf_kl_forward_workspace", "hdf_kl_forward")
 
 
 class HdfError(RuntimeError):
@@ -111,6 +111,11 @@ def lib() -> ctypes.CDLL:
     L.hdf_accept_sample.restype = _I
     L.hdf_accept_sample.argtypes = [_P, _I, _P, _P, _I64, _P, _I, _I, _I, _F, _U64, _U64, _P, _P,
                                     _P, _P, _P, _SZ, _P]
+    L.hdf_kl_forward_workspace.restype = _SZ
+    L.hdf_kl_forward_workspace.argtypes = [_I, _I, _I, _I, _I, _I]
+    L.hdf_kl_forward.restype = _I
+    L.hdf_kl_forward.argtypes = [_P, _I, _P, _F, _P, _I, _I, _I, _P, _I64, _I, _P, _I, _I, _F, _F,
+                                 _P, _P, _P, _P, _SZ, _P]
     _lib = L
     return L
 
@@ -251,6 +256,34 @@ def accept_sample(draft: torch.Tensor, draft_logits: torch.Tensor, draft_lse: to
                                    int(seed), int(stream_id), _ptr(acc), _ptr(anc), _ptr(offs),
                                    _ptr(toks), _ptr(ws), ws.numel(), _stream(stream)))
     return acc, anc, offs, toks
+
+
+def kl_forward(H_pos: torch.Tensor, w_lm: "PackedWeight", student_logits: torch.Tensor, *,
+               B: int, P: int, gamma: Optional[torch.Tensor] = None, eps: float = 1e-6,
+               labels: Optional[torch.Tensor] = None, temperature: float = 1.0,
+               alpha: float = 0.1, ws=None, stream=None):
+    """hdf_kl_forward: H_pos [n_seq, P, m, d], student_logits [n_seq*B, V] fp32 ->
+    (kl [n_seq, P], ce [n_seq, B-1] or None, loss [3] = L_KL, L_CE, L)."""
+    n_seq, P_, m, d = H_pos.shape
+    if P_ != P:
+        raise ValueError("H_pos must hold P positions per block")
+    V = w_lm.N
+    dev = H_pos.device
+    kl = torch.empty((n_seq, P), dtype=torch.float32, device=dev)
+    ce = torch.empty((n_seq, B - 1), dtype=torch.float32, device=dev) if labels is not None else None
+    loss = torch.empty(3, dtype=torch.float32, device=dev)
+    need = int(lib().hdf_kl_forward_workspace(n_seq, B, P, d, V, _dt(H_pos)))
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    if student_logits.dtype != torch.float32 or student_logits.stride(1) != 1:
+        raise ValueError("student_logits must be fp32 with unit column stride")
+    _dev(H_pos, w_lm.data, gamma, labels, kl, ws)
+    _check(lib().hdf_kl_forward(_ptr(H_pos), m, _ptr(gamma), float(eps), w_lm.data_ptr(), d, V,
+                                _dt(H_pos), _ptr(student_logits), student_logits.stride(0), B,
+                                _ptr(labels), n_seq, P, float(temperature), float(alpha),
+                                _ptr(kl), _ptr(ce), _ptr(loss), _ptr(ws), ws.numel(),
+                                _stream(stream)))
+    return kl, ce, loss
 
 
 # ----------------------------------------------------------------------------- weights
