@@ -52,6 +52,8 @@ def parse():
     ap.add_argument("--temperature", type=float, default=0.0, metavar="T",
                     help="also time the step at temperature T > 0 (draws from softmax(z / T) and "
                          "speculative-sampling verification against synthetic target logits)")
+    ap.add_argument("--kl", action="store_true",
+                    help="also time the KL-distillation forward on the full-size blocks")
     ap.add_argument("--fc-reducer", action="store_true",
                     help="also time the generic fc reducer beside the gated one (warm-step "
                          "rows and the reducer-stress shape)")
@@ -248,20 +250,49 @@ def sampled_leg(torch, synth, hdf, wl, h, bufs, args, T, steps, warmup):
     for r in range(warmup):
         drafter_step_sampled(h, bufs, sb, target_logits=tgt, temperature=T, round_id=r, **kw)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    accs = []
+    accs = torch.empty((steps, n_seq), dtype=torch.int32, device="cuda")
     torch.cuda.synchronize()
     e0.record()
     for r in range(steps):
         out = drafter_step_sampled(h, bufs, sb, target_logits=tgt, temperature=T,
                                    round_id=warmup + r, **kw)
-        accs.append(out["accept_len"])
+        accs[r].copy_(out["accept_len"])
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
-    acc = torch.stack(accs).float()
+    acc = accs.float()
     res = {"temperature": T, "ms_per_step": round(ms, 4), "blocks_per_s": round(n_seq / (ms * 1e-3), 1),
            "steps": steps, "mean_accept_len": round(float(acc.mean()), 3)}
     del sb, tgt
+    torch.cuda.empty_cache()
+    return res
+
+
+def kl_leg(torch, synth, hdf, wl, h):
+    """hdf_kl_forward on the full-size blocks (8 x 16 slots, P = 2, vocabulary 129280):
+    the teacher LM head over 16 pooled target states, the KL and cross-entropy passes.
+    HIP events around 10 calls."""
+    n, B, P, m, d, V = wl.n_seq, wl.block, 2, wl.m, wl.d, h.V
+    H = synth.normal([n, P, m, d], 1.0, wl.seed, 80, device="cuda")
+    g = torch.Generator(device="cuda").manual_seed(wl.seed)
+    z = torch.randn((n * B, V), generator=g, device="cuda")
+    lab = torch.randint(0, V, (n, B - 1), generator=g, device="cuda").to(torch.int32)
+    ws = torch.empty(int(hdf.lib().hdf_kl_forward_workspace(n, B, P, d, V, hdf.HDF_BF16)),
+                     dtype=torch.uint8, device="cuda")
+    fn = lambda: hdf.kl_forward(H, h.w_lm, z, B=B, P=P, labels=lab, temperature=1.0, alpha=0.1,
+                                ws=ws)
+    for _ in range(2):
+        fn()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(10):
+        out = fn()
+    e1.record()
+    torch.cuda.synchronize()
+    res = {"n_seq": n, "B": B, "P": P, "vocab": V, "us": round(e0.elapsed_time(e1) / 10 * 1e3, 1),
+           "loss": [round(float(x), 4) for x in out[2].cpu()]}
+    del H, z, lab, ws
     torch.cuda.empty_cache()
     return res
 
@@ -510,6 +541,8 @@ def main():
     if a.temperature > 0:
         res["sampled_step"] = sampled_leg(torch, synth, hdf, wl, h, bufs, args, a.temperature,
                                           a.steps, 3)
+    if a.kl:
+        res["kl_forward"] = kl_leg(torch, synth, hdf, wl, h)
     if a.fc_reducer:
         res["fc_reducer"] = fc_reducer_leg(torch, synth, hdf)
     if a.blas_ref:
