@@ -12,36 +12,50 @@
 // page page_table[s][j]; its block keys sit in 64-row slot s of separate block buffers
 // of the same layout.
 //
-// bf16 kernel: grid (context chunk + 1 block chunk, head, sequence x 16-query
-// group), 4 waves.  A wave streams 64-key tiles and keeps its 16 queries' state
-// in registers:
+// bf16 kernel: grid (chunk, head, sequence x 16-query group), NW = 4 or 8 waves.
+// With one chunk (n_chunks == 1) a workgroup takes all of its sequence's context
+// tiles and the block's tile and writes the normalised output rows.  Otherwise
+// chunks 0 .. n_chunks-1 take chunk_len context keys each and chunk n_chunks the
+// block's tile, every one writes a partial (O, m, l), and a combine kernel merges
+// them (log-sum-exp rescaling).  Wave w takes tiles w, w + NW, ...  A wave keeps its 16
+// queries' state in registers:
 //   S^T (keys x queries) = K . Q^T     v_mfma_f32_16x16x32_bf16, Q as the B operand
 //   O^T (hd x queries)  += V^T . P^T   same instruction, V^T as the A operand, P^T
 //                                      as a bf16 hi + lo pair
 // Keys inside each 32-key step are ordered so that the S^T accumulator a lane
 // holds (4 keys of one query per 16-key sub-tile) is exactly the 8 keys of one
-// query the P^T operand needs, so P never leaves registers.  No LDS in the key loop.  The four
-// waves of a workgroup merge through LDS at the end; chunks merge in a combine
-// kernel (log-sum-exp rescaling).
+// query the P^T operand needs, so P never leaves registers.  The key loop reads no
+// LDS and issues no dependent global loads (the chunk's cache tiles are looked up
+// once, into LDS, before it); the two waves of a SIMD overlap one's loads with the
+// other's products.  The waves of a workgroup merge through LDS at the end.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace hdf {
 
-constexpr int kAttnThreads = 256;
-constexpr int kAttnWaves = 4;
+constexpr int kCombineThreads = 256;
 constexpr int kKeyTile = 64;
+constexpr int kMaxChunkTiles = kAttnMaxChunk / kKeyTile;
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-template <int HD>
-__global__ void __launch_bounds__(kAttnThreads)
-attn_bf16_kernel(AttnArgs a) {
+// Context chunks of a sequence of T cached positions.
+__device__ __forceinline__ int attn_ctx_chunks(const AttnArgs& a, int T) {
+  return min(a.n_chunks, (T + a.chunk_len - 1) / a.chunk_len);
+}
+
+// Two waves per SIMD: 256 VGPRs per wave at most.
+template <int HD, int NW>
+__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)))
+attn_bf16_kernel(AttnArgs a, bf16_t* __restrict__ out) {
+  constexpr int kAttnWaves = NW;
+  constexpr int kAttnThreads = 64 * NW;
   constexpr int NJ = HD / 32;   // MFMA steps over the head dimension for S
   constexpr int NDT = HD / 16;  // 16-row tiles of O^T
   __shared__ float red_o[kAttnWaves][16][HD + 1];
   __shared__ float red_m[kAttnWaves][16];
   __shared__ float red_l[kAttnWaves][16];
+  __shared__ int64_t ctile[kMaxChunkTiles];   // cache tile of each context tile of the chunk
 
   const int chunk = blockIdx.x;
   const int h = blockIdx.y;
@@ -53,32 +67,39 @@ attn_bf16_kernel(AttnArgs a) {
   const int g = lane >> 4;       // lane group 0..3
   const int ql = lane & 15;      // query within the group / row within a sub-tile
   const int T = a.ctx_len[s];
+  const bool direct = a.n_chunks == 1;
+  const bool blk_chunk = chunk == a.n_chunks;   // the block's own workgroup
+  if (!direct && !blk_chunk && chunk >= attn_ctx_chunks(a, T)) return;  // past the context
 
-  // 64-row tiles of this head's keys (values): tile j of the segment is tile
-  // tile0 + j, or page pt[j] of a paged cache.
-  const bf16_t* khead;
-  const bf16_t* vhead;
-  const int32_t* pt = nullptr;
-  int64_t tile0 = 0;
-  int k_lo, k_hi;
-  if (chunk < a.n_chunks) {
-    k_lo = chunk * a.chunk_len;
-    if (k_lo >= T) return;  // nothing of this sequence in this chunk
-    k_hi = min(T, k_lo + a.chunk_len);
-    khead = static_cast<const bf16_t*>(a.kc) + int64_t(h) * a.cap * HD;
-    vhead = static_cast<const bf16_t*>(a.vtc) + int64_t(h) * a.cap * HD;
-    if (a.page_table != nullptr)
-      pt = a.page_table + int64_t(s) * a.max_pages;
-    else
-      tile0 = a.kv_offsets[s] >> 6;
+  // Context keys [k_lo, k_hi) of the chunk in 64-row tiles (the sequence's tile t is
+  // cache tile kv_offsets[s]/64 + t, or page page_table[s][t] of a paged cache); the
+  // block's tile (B keys, slot s of the block buffers) follows them.
+  const int k_lo = blk_chunk ? 0 : min(T, chunk * a.chunk_len);
+  const int k_hi = blk_chunk ? 0 : min(T, k_lo + a.chunk_len);
+  const int nct = (k_hi - k_lo + kKeyTile - 1) / kKeyTile;
+  const int ntiles = nct + ((direct || blk_chunk) ? 1 : 0);
+  const bf16_t* kch = static_cast<const bf16_t*>(a.kc) + int64_t(h) * a.cap * HD;
+  const bf16_t* vch = static_cast<const bf16_t*>(a.vtc) + int64_t(h) * a.cap * HD;
+  const bf16_t* kbh = static_cast<const bf16_t*>(a.kb) + int64_t(h) * a.capb * HD + lane * 8;
+  const bf16_t* vbh = static_cast<const bf16_t*>(a.vtb) + int64_t(h) * a.capb * HD + lane * 8;
+  // The chunk's cache tiles go to LDS first, so the key loop has no dependent global
+  // loads (each would make a wave wait for all of its outstanding tile loads).
+  if (a.page_table != nullptr) {
+    const int32_t* pt = a.page_table + int64_t(s) * a.max_pages + (k_lo >> 6);
+    for (int j = threadIdx.x; j < nct; j += kAttnThreads) ctile[j] = pt[j];
   } else {
-    k_lo = 0;
-    k_hi = a.B;
-    khead = static_cast<const bf16_t*>(a.kb) + int64_t(h) * a.capb * HD;
-    vhead = static_cast<const bf16_t*>(a.vtb) + int64_t(h) * a.capb * HD;
-    tile0 = s;
+    const int64_t t0 = (a.kv_offsets[s] >> 6) + (k_lo >> 6);
+    for (int j = threadIdx.x; j < nct; j += kAttnThreads) ctile[j] = t0 + j;
   }
-  auto tile_of = [&](int t) -> int64_t { return pt != nullptr ? int64_t(pt[t >> 6]) : tile0 + (t >> 6); };
+  __syncthreads();
+  // Tile i's first operand (plus this lane's 16 bytes) and its number of valid keys.
+  auto k_src = [&](int i) -> const bf16_t* {
+    return i >= nct ? kbh + int64_t(s) * 64 * HD : kch + ctile[i] * 64 * HD + lane * 8;
+  };
+  auto v_src = [&](int i) -> const bf16_t* {
+    return i >= nct ? vbh + int64_t(s) * 64 * HD : vch + ctile[i] * 64 * HD + lane * 8;
+  };
+  auto valid_of = [&](int i) { return i >= nct ? a.B : min(kKeyTile, k_hi - k_lo - i * kKeyTile); };
 
   // Q^T operand: lane holds Q[query ql][32j + 8g .. +7].
   const int q = qg * 16 + ql;
@@ -98,29 +119,31 @@ attn_bf16_kernel(AttnArgs a) {
   float m_run = -INFINITY;
   float l_run = 0.f;
 
-  // The tile of the next iteration is looked up one iteration ahead.
-  int64_t tile = (k_lo + wid * kKeyTile < k_hi) ? tile_of(k_lo + wid * kKeyTile) : 0;
-  for (int t0 = k_lo + wid * kKeyTile; t0 < k_hi; t0 += kAttnWaves * kKeyTile) {
-    const int tn = t0 + kAttnWaves * kKeyTile;
-    const int64_t tile_next = tn < k_hi ? tile_of(tn) : 0;
-    // K operands of the four 16-key sub-tiles: sub-tile st = 2*ks + p, row r -> key
-    // t0 + 32ks + 8(r/4) + 4p + r%4 (the order of the cache tile layout).
-    // In the cache tile layout each operand is 64 lanes x 16 contiguous bytes.
-    const bf16_t* ktile = khead + tile * 64 * HD + lane * 8;
-    bf16x8_t kf[4][NJ];
+  // K operands of the four 16-key sub-tiles: sub-tile st = 2*ks + p, row r -> key
+  // 32ks + 8(r/4) + 4p + r%4 of the tile (the order of the cache tile layout); each
+  // operand is 64 lanes x 16 contiguous bytes.  V^T operands: lane holds
+  // V^T[16dt + ql][32ks + 8g .. +7].
+  bf16x8_t kf[4][NJ];
+  u32x4 vf[2][NDT];
+  auto load_k = [&](int i) {
+    const bf16_t* kt = k_src(i);
 #pragma unroll
     for (int st = 0; st < 4; ++st)
 #pragma unroll
       for (int j = 0; j < NJ; ++j)
-        kf[st][j] = __builtin_bit_cast(bf16x8_t, ld16(ktile + (st * NJ + j) * 512));
-    // V^T operands: lane holds V^T[16dt + ql][t0 + 32ks + 8g .. +7].
-    const bf16_t* vtile = vhead + tile * 64 * HD + lane * 8;
-    u32x4 vf[2][NDT];
+        kf[st][j] = __builtin_bit_cast(bf16x8_t, ld16(kt + (st * NJ + j) * 512));
+  };
+  auto load_v = [&](int i) {
+    const bf16_t* vt = v_src(i);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) vf[ks][dt] = ld16(vtile + (ks * NDT + dt) * 512);
-
+      for (int dt = 0; dt < NDT; ++dt) vf[ks][dt] = ld16(vt + (ks * NDT + dt) * 512);
+  };
+  for (int i = wid; i < ntiles; i += kAttnWaves) {
+    load_k(i);
+    load_v(i);
+    const int nval = valid_of(i);
     float sv[4][4];
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
@@ -129,16 +152,16 @@ attn_bf16_kernel(AttnArgs a) {
       for (int j = 0; j < NJ; ++j)
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[st][j], qf[j], acc, 0, 0, 0);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = t0 + 32 * (st >> 1) + 8 * g + 4 * (st & 1) + i;
-        sv[st][i] = (key < k_hi) ? acc[i] * a.scale_log2 : -INFINITY;
+      for (int e = 0; e < 4; ++e) {
+        const int key = 32 * (st >> 1) + 8 * g + 4 * (st & 1) + e;
+        sv[st][e] = (key < nval) ? acc[e] * a.scale_log2 : -INFINITY;
       }
     }
     float tmax = -INFINITY;
 #pragma unroll
     for (int st = 0; st < 4; ++st)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) tmax = fmaxf(tmax, sv[st][i]);
+      for (int e = 0; e < 4; ++e) tmax = fmaxf(tmax, sv[st][e]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
     const float m_new = fmaxf(m_run, tmax);   // finite: every tile has a valid key
@@ -149,57 +172,56 @@ attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
     for (int st = 0; st < 4; ++st)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        pv[st][i] = fast_exp2(sv[st][i] - m_new);
-        psum += pv[st][i];
+      for (int e = 0; e < 4; ++e) {
+        pv[st][e] = fast_exp2(sv[st][e] - m_new);
+        psum += pv[st][e];
       }
     l_run = l_run * alpha + psum;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) oacc[dt][i] *= alpha;
+      for (int e = 0; e < 4; ++e) oacc[dt][e] *= alpha;
 
+    // Keys past the valid ones carry P = 0; zero their V too (the slot padding is never
+    // written and may hold anything).  Only a segment's last tile is partial; its V
+    // operands are masked in place (lane keys 32ks + 8g .. +7).
+    if (nval < kKeyTile) {
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const int nvalid = nval - (32 * ks + 8 * g);
+        uint32_t keep[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          keep[e] = ((2 * e < nvalid) ? 0x0000FFFFu : 0u) | ((2 * e + 1 < nvalid) ? 0xFFFF0000u : 0u);
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) vf[ks][dt][e] &= keep[e];
+      }
+    }
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       // P^T operand: keys 32ks + 8g + 0..7 of query ql, as a bf16 pair hi + lo
       // (P carries ~16 significant bits into the fp32 accumulation; the key loop is
       // HBM-bound, so the second MFMA is free).
-      float pk[8];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        pk[i] = pv[2 * ks][i];
-        pk[4 + i] = pv[2 * ks + 1][i];
-      }
       uint32_t hw[4], lw[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const bf16_t h0 = f2bf(pk[2 * e]), h1 = f2bf(pk[2 * e + 1]);
+        const float p0 = pv[2 * ks + (e >> 1)][2 * (e & 1)];
+        const float p1 = pv[2 * ks + (e >> 1)][2 * (e & 1) + 1];
+        const bf16_t h0 = f2bf(p0), h1 = f2bf(p1);
         hw[e] = uint32_t(h0) | (uint32_t(h1) << 16);
-        lw[e] = pack_bf2(pk[2 * e] - bf2f(h0), pk[2 * e + 1] - bf2f(h1));
+        lw[e] = pack_bf2(p0 - bf2f(h0), p1 - bf2f(h1));
       }
       const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, u32x4{hw[0], hw[1], hw[2], hw[3]});
       const bf16x8_t pf_lo = __builtin_bit_cast(bf16x8_t, u32x4{lw[0], lw[1], lw[2], lw[3]});
-      // Keys past the segment end carry P = 0; zero their V too (the slot padding
-      // is never written and may hold anything).
-      const int kfirst = t0 + 32 * ks + 8 * g;
-      const int nvalid = k_hi - kfirst;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
-        u32x4 v = vf[ks][dt];
-        if (nvalid < 8) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const uint32_t keep_lo = (2 * e < nvalid) ? 0x0000FFFFu : 0u;
-            const uint32_t keep_hi = (2 * e + 1 < nvalid) ? 0xFFFF0000u : 0u;
-            v[e] &= (keep_lo | keep_hi);
-          }
-        }
-        const bf16x8_t vop = __builtin_bit_cast(bf16x8_t, v);
+        const bf16x8_t vop = __builtin_bit_cast(bf16x8_t, vf[ks][dt]);
         oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pf, oacc[dt], 0, 0, 0);
         oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pf_lo, oacc[dt], 0, 0, 0);
       }
     }
-    tile = tile_next;
   }
 
   // Wave -> LDS: lane (g, ql) holds O^T[16dt + 4g + i][ql].
@@ -212,26 +234,37 @@ attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) red_o[wid][ql][16 * dt + 4 * g + i] = oacc[dt][i];
+    for (int e = 0; e < 4; ++e) red_o[wid][ql][16 * dt + 4 * g + e] = oacc[dt][e];
   __syncthreads();
 
+  // Merge of the waves: thread -> (query qq, two consecutive dims).
   const int64_t pidx = ((int64_t(s) * a.nh + h) * (a.n_chunks + 1) + chunk) * a.QB + qg * 16;
-  for (int e = threadIdx.x; e < 16 * HD; e += kAttnThreads) {
-    const int qq = e / HD, dim = e - qq * HD;
+  for (int e = threadIdx.x; e < 16 * (HD / 2); e += kAttnThreads) {
+    const int qq = e / (HD / 2), dim = 2 * (e - qq * (HD / 2));
     float mm = red_m[0][qq];
 #pragma unroll
     for (int w = 1; w < kAttnWaves; ++w) mm = fmaxf(mm, red_m[w][qq]);
-    float o = 0.f, l = 0.f;
+    float o0 = 0.f, o1 = 0.f, l = 0.f;
 #pragma unroll
     for (int w = 0; w < kAttnWaves; ++w) {
       const float f = (red_m[w][qq] == -INFINITY) ? 0.f : fast_exp2(red_m[w][qq] - mm);
-      o += f * red_o[w][qq][dim];
+      o0 += f * red_o[w][qq][dim];
+      o1 += f * red_o[w][qq][dim + 1];
       l += f * red_l[w][qq];
     }
-    a.part_o[(pidx + qq) * HD + dim] = o;
-    if (dim == 0) {
-      a.part_ml[(pidx + qq) * 2 + 0] = mm;
-      a.part_ml[(pidx + qq) * 2 + 1] = l;
+    if (direct) {
+      const int qo = qg * 16 + qq;
+      if (qo < a.B) {
+        const float inv = 1.f / l;
+        *reinterpret_cast<uint32_t*>(out + (int64_t(s) * a.B + qo) * (a.nh * HD) +
+                                     int64_t(h) * HD + dim) = pack_bf2(o0 * inv, o1 * inv);
+      }
+    } else {
+      *reinterpret_cast<float2*>(a.part_o + (pidx + qq) * HD + dim) = make_float2(o0, o1);
+      if (dim == 0) {
+        a.part_ml[(pidx + qq) * 2 + 0] = mm;
+        a.part_ml[(pidx + qq) * 2 + 1] = l;
+      }
     }
   }
 }
@@ -240,24 +273,23 @@ attn_bf16_kernel(AttnArgs a) {
 // Phase 1 reads every chunk's (m, l), phase 2 turns them into per-chunk weights
 // exp2(m_c - M) / L, phase 3 forms each output quad from independent loads.
 template <typename T>
-__global__ void __launch_bounds__(kAttnThreads)
+__global__ void __launch_bounds__(kCombineThreads)
 attn_combine_kernel(AttnArgs a, T* __restrict__ out) {
   extern __shared__ float cw[];  // [16][n_chunks + 1] weights, then [16][n_chunks + 1] m
   const int h = blockIdx.y;
   const int nqg = (a.B + 15) / 16;
   const int s = blockIdx.x / nqg;
   const int qg = blockIdx.x - s * nqg;
-  const int T_s = a.ctx_len[s];
-  const int nc = min(a.n_chunks, (T_s + a.chunk_len - 1) / a.chunk_len);
+  const int nc = attn_ctx_chunks(a, a.ctx_len[s]) + 1;   // context chunks + the block's
   const int NC = a.n_chunks + 1;
   float* cm = cw + 16 * NC;
   const int d = a.nh * a.hd;
   const int64_t base = (int64_t(s) * a.nh + h) * NC;
-  // Phase 1: (m, l) of every used chunk (nc context chunks, then the block chunk).
-  for (int e = threadIdx.x; e < 16 * (nc + 1); e += kAttnThreads) {
-    const int qq = e / (nc + 1);
-    const int c = e - qq * (nc + 1);
-    const int cc = (c == nc) ? a.n_chunks : c;
+  // Phase 1: (m, l) of every chunk of the sequence (the block's is chunk n_chunks).
+  for (int e = threadIdx.x; e < 16 * nc; e += kCombineThreads) {
+    const int qq = e / nc;
+    const int c = e - qq * nc;
+    const int cc = (c == nc - 1) ? a.n_chunks : c;
     const int64_t pi = (base + cc) * a.QB + qg * 16 + qq;
     cm[qq * NC + c] = a.part_ml[pi * 2];
     cw[qq * NC + c] = a.part_ml[pi * 2 + 1];
@@ -267,28 +299,28 @@ attn_combine_kernel(AttnArgs a, T* __restrict__ out) {
   if (threadIdx.x < 16) {
     const int qq = threadIdx.x;
     float mm = -INFINITY;
-    for (int c = 0; c <= nc; ++c) mm = fmaxf(mm, cm[qq * NC + c]);
+    for (int c = 0; c < nc; ++c) mm = fmaxf(mm, cm[qq * NC + c]);
     float l = 0.f;
-    for (int c = 0; c <= nc; ++c) {
+    for (int c = 0; c < nc; ++c) {
       const float f = (cm[qq * NC + c] == -INFINITY) ? 0.f : fast_exp2(cm[qq * NC + c] - mm);
       cm[qq * NC + c] = f;
       l += f * cw[qq * NC + c];
     }
     const float inv = 1.f / l;
-    for (int c = 0; c <= nc; ++c) cw[qq * NC + c] = cm[qq * NC + c] * inv;
+    for (int c = 0; c < nc; ++c) cw[qq * NC + c] = cm[qq * NC + c] * inv;
   }
   __syncthreads();
   // Phase 3: outputs, four consecutive dims per item.
   const int quads = a.hd / 4;
-  for (int e = threadIdx.x; e < 16 * quads; e += kAttnThreads) {
+  for (int e = threadIdx.x; e < 16 * quads; e += kCombineThreads) {
     const int qq = e / quads;
     const int q = qg * 16 + qq;
     if (q >= a.B) continue;
     const int i0 = (e - qq * quads) * 4;
     float o[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int c = 0; c <= nc; ++c) {
-      const int cc = (c == nc) ? a.n_chunks : c;
+    for (int c = 0; c < nc; ++c) {
       const float wgt = cw[qq * NC + c];
+      const int cc = (c == nc - 1) ? a.n_chunks : c;
       const float4 v = *reinterpret_cast<const float4*>(
           a.part_o + ((base + cc) * a.QB + q) * a.hd + i0);
       o[0] = fmaf(wgt, v.x, o[0]);
@@ -371,17 +403,25 @@ hipError_t launch_attention(bool bf16, const AttnArgs& a, void* out, hipStream_t
                          static_cast<float*>(out));
     return hipGetLastError();
   }
+  if (a.n_chunks < 1 || a.chunk_len % kKeyTile != 0 || a.chunk_len > kAttnMaxChunk ||
+      (a.waves != 4 && a.waves != 8))
+    return hipErrorInvalidValue;
   const int nqg = (a.B + 15) / 16;
-  const dim3 grid(a.n_chunks + 1, a.nh, a.n_seq * nqg);
-  if (a.hd == 128)
-    hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(kAttnThreads), 0, s, a);
-  else
-    hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(kAttnThreads), 0, s, a);
+  const dim3 grid(a.n_chunks == 1 ? 1 : a.n_chunks + 1, a.nh, a.n_seq * nqg);
+  bf16_t* o = static_cast<bf16_t*>(out);
+  const bool w8 = a.waves == 8;
+  if (a.hd == 128) {
+    if (w8) hipLaunchKernelGGL((attn_bf16_kernel<128, 8>), grid, dim3(512), 0, s, a, o);
+    else hipLaunchKernelGGL((attn_bf16_kernel<128, 4>), grid, dim3(256), 0, s, a, o);
+  } else {
+    if (w8) hipLaunchKernelGGL((attn_bf16_kernel<64, 8>), grid, dim3(512), 0, s, a, o);
+    else hipLaunchKernelGGL((attn_bf16_kernel<64, 4>), grid, dim3(256), 0, s, a, o);
+  }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || a.n_chunks == 1) return e;
   const size_t lds = size_t(2) * 16 * (a.n_chunks + 1) * sizeof(float);
-  hipLaunchKernelGGL(attn_combine_kernel<bf16_t>, dim3(a.n_seq * nqg, a.nh), dim3(kAttnThreads),
-                     lds, s, a, static_cast<bf16_t*>(out));
+  hipLaunchKernelGGL(attn_combine_kernel<bf16_t>, dim3(a.n_seq * nqg, a.nh), dim3(kCombineThreads),
+                     lds, s, a, o);
   return hipGetLastError();
 }
 

@@ -173,10 +173,14 @@ struct AttnArgs {
   int64_t capb;
   int n_seq, nh, hd, B, QB;  // QB = B rounded up to 16
   int n_chunks, chunk_len;   // context chunks of the grid (chunk_len % 64 == 0)
+  int waves;                 // waves per workgroup of the bf16 kernel (4 or 8)
   float scale_log2;          // log2(e) / sqrt(hd)
   float* part_o;             // [n_seq][nh][n_chunks+1][QB][hd]
   float* part_ml;            // [n_seq][nh][n_chunks+1][QB][2]
 };
+
+// Longest context chunk of one bf16 attention workgroup.
+constexpr int kAttnMaxChunk = 16384;
 
 // out: [n_seq*B][nh*hd] attention output rows in the working dtype.
 hipError_t launch_attention(bool bf16, const AttnArgs& a, void* out, hipStream_t s);
