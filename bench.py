@@ -170,8 +170,9 @@ def decode_leg(torch, synth, hdf, rounds, warmup):
     shuffled order), a first round projecting the last 16, then one round after another
     appending each sequence's n_s + 1 committed positions.  The target model is stood in
     for by device-side tokens that copy each draft with probability 0.8.  Timed: the
-    rounds end to end, with the page bookkeeping and the per-round read of the
-    accepted lengths the host needs."""
+    rounds end to end with their page bookkeeping, twice: chained on the device (the
+    accepted lengths never leave it; the host takes pages ahead of an upper bound) and,
+    for comparison, with the host reading the accepted lengths back after every round."""
     import numpy as np
     from paper_2606_26744_amd.decode import PagedDecoder
     wl = synth.drafter_full()
@@ -185,27 +186,40 @@ def decode_leg(torch, synth, hdf, rounds, warmup):
                           rope_theta=dr.rope_theta, rope_max_pos=max_ctx + B)
     n_pages = n_seq * ((max_ctx + 63) // 64) + 8
     order = np.random.default_rng(wl.seed).permutation(n_pages)
-    dec = PagedDecoder(h, n_seq, B, max_ctx, n_pages, n_seq * B, page_order=order)
     pre = T0 - wl.new_rows
-    dec.preload(np.full(n_seq, pre, dtype=np.int64))     # the cached prefix of every sequence
-    for s in range(n_seq):
-        for l in range(dr.n_layers):
-            k, v = synth.kv_prefix(wl, pre, l, device="cuda", sub=s)
-            hdf.write_kv_rows_paged(dec.kv_k, dec.kv_vt, l, dec.pages[s], k, v)
-            del k, v
-    dec.set_anchors(synth.block_tokens(wl, device="cuda")[:, 0])
     red = synth.reducer_inputs(wl, n_seq * B, device="cuda")
     V, p = dr.vocab, 0.8
     gen = torch.Generator(device="cuda").manual_seed(wl.seed)
+    # The target's draws of every round, made before the timed rounds: whether it keeps
+    # each draft (probability p), the token it has instead (uniform; equal to the draft
+    # with probability 1/V) and the token after the block.
+    n_rounds = 2 * (warmup + rounds)
+    keep = torch.rand((n_rounds, n_seq, B - 1), generator=gen, device="cuda") < p
+    other = torch.randint(0, V, (n_rounds, n_seq, B - 1), generator=gen, device="cuda",
+                          dtype=torch.int32)
+    tgt = torch.randint(0, V, (n_rounds, n_seq, B), generator=gen, device="cuda",
+                        dtype=torch.int32)
+    rnd = [0]
 
     def targets(drafts):
-        n, K = drafts.shape
-        u = torch.rand((n, K), generator=gen, device="cuda")
-        other = ((drafts.long() + 1 + torch.randint(0, V - 1, (n, K), generator=gen,
-                                                      device="cuda")) % V).to(torch.int32)
-        bonus = torch.randint(0, V, (n, 1), generator=gen, device="cuda").to(torch.int32)
-        return torch.cat([torch.where(u < p, drafts, other), bonus], dim=1).contiguous()
+        r = rnd[0]
+        rnd[0] += 1
+        tgt[r, :, :B - 1].copy_(torch.where(keep[r], drafts, other[r]))
+        return tgt[r]
 
+    def decoder():
+        dec = PagedDecoder(h, n_seq, B, max_ctx, n_pages, n_seq * B, page_order=order)
+        dec.preload(np.full(n_seq, pre, dtype=np.int64))     # the cached prefix of every sequence
+        for s in range(n_seq):
+            for l in range(dr.n_layers):
+                k, v = synth.kv_prefix(wl, pre, l, device="cuda", sub=s)
+                hdf.write_kv_rows_paged(dec.kv_k, dec.kv_vt, l, dec.pages[s], k, v)
+                del k, v
+        dec.set_anchors(synth.block_tokens(wl, device="cuda")[:, 0])
+        return dec
+
+    # host-synchronised rounds
+    dec = decoder()
     counts = np.full(n_seq, wl.new_rows, dtype=np.int64)
 
     def one(counts):
@@ -222,12 +236,36 @@ def decode_leg(torch, synth, hdf, rounds, warmup):
         counts = one(counts)
         committed += int(counts.sum())
     torch.cuda.synchronize()
+    dt_sync = time.perf_counter() - t0
+    sync_res = {"ms_per_round": round(dt_sync / rounds * 1e3, 4),
+                "blocks_per_s": round(n_seq * rounds / dt_sync, 1),
+                "committed_tokens_per_s": round(committed / dt_sync, 1),
+                "mean_accept_len": round(committed / (rounds * n_seq) - 1, 3)}
+    del dec
+    torch.cuda.empty_cache()
+
+    # chained rounds
+    dec = decoder()
+    dec.start_chain(np.full(n_seq, wl.new_rows, dtype=np.int64))
+    H = red["H"][:n_seq * B]
+    for _ in range(warmup):
+        dec.chained_round(H, red["W_g"], red["b_g"], targets)
+    torch.cuda.synchronize()
+    c0 = dec.sync_lengths()
+    t0 = time.perf_counter()
+    for _ in range(rounds):
+        dec.chained_round(H, red["W_g"], red["b_g"], targets)
+    torch.cuda.synchronize()
     dt = time.perf_counter() - t0
-    res = {"n_seq": n_seq, "rounds": rounds, "ms_per_round": round(dt / rounds * 1e3, 4),
+    c1 = dec.sync_lengths()
+    committed = int((c1 - c0).sum())
+    res = {"n_seq": n_seq, "rounds": rounds, "mode": "chained on the device",
+           "ms_per_round": round(dt / rounds * 1e3, 4),
            "blocks_per_s": round(n_seq * rounds / dt, 1),
            "committed_tokens_per_s": round(committed / dt, 1),
            "mean_accept_len": round(committed / (rounds * n_seq) - 1, 3),
-           "context_end": [int(x) for x in dec.ctx], "pages_used": n_pages - dec.pool.free}
+           "context_end": [int(x) for x in c1], "pages_used": n_pages - dec.pool.free,
+           "host_synchronised": sync_res}
     del dec, h, w, red
     torch.cuda.empty_cache()
     return res

@@ -8,7 +8,8 @@
  *                          (Sec. 1, Sec. 2.1; slot alignment of Sec. 2.3)
  *   3. hdf_lm_head_argmax  draft logits z_k and greedy draft tokens (Sec. 2.3)
  *   4. hdf_accept          greedy verification: longest agreeing prefix (Sec. 1, Sec. 3.4)
- *      (hdf_sample_tokens, hdf_accept_sample: the same at temperature T > 0)
+ *      (hdf_sample_tokens, hdf_accept_sample: the same at temperature T > 0;
+ *       hdf_advance_context: the committed positions become the next round's context)
  *
  * Conventions shared by every call:
  *   - Tensor arguments are DEVICE pointers unless marked "host".  Tensors are dense,
@@ -246,10 +247,21 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
  *             past a sequence's last page are not read.  Not checked on the device.
  * max_pages   host: row stride of page_table; max_pages * 64 >= max_ctx
  * kv_pages    host: pages in the pool (kv_pages * 64 < 2^31)
+ * new_counts  [n_seq] int32 (device) or NULL.  NULL: every row new_offsets[s] ..
+ *             new_offsets[s+1]-1 is new, as in hdf_draft_block.  Given: only the first
+ *             min(new_counts[s], new_offsets[s+1] - new_offsets[s]) rows of sequence s are
+ *             new, its positions T_s - n_s .. T_s - 1 with that n_s; its other rows are
+ *             read but neither projected into the cache nor used.  This lets a chained
+ *             decode loop size the call for an upper bound (B rows per sequence, every
+ *             sequence committing at most B positions a round) while the counts come
+ *             from the device (hdf_advance_context after hdf_accept), so the host never
+ *             waits for the accepted lengths.  A row whose position would fall outside
+ *             [0, max_pages * 64) is skipped likewise.
  * Every other argument and limit is that of hdf_draft_block. */
 hdf_status hdf_draft_block_paged(const hdf_drafter* w, int n_seq, int B, const int32_t* ctx_len,
                                  int max_ctx, const void* y_new, const int32_t* new_offsets,
-                                 int64_t n_new, const int32_t* page_table, int max_pages,
+                                 const int32_t* new_counts, int64_t n_new,
+                                 const int32_t* page_table, int max_pages,
                                  void* kv_k, void* kv_vt, int64_t kv_pages,
                                  const int32_t* tokens, void* hidden, void* ws, size_t ws_bytes,
                                  hdf_stream_t stream);
@@ -300,6 +312,18 @@ hdf_status hdf_lm_head_argmax(const void* hidden, const void* W_lm, int64_t M, i
 hdf_status hdf_accept(const int32_t* draft, int draft_stride, const int32_t* target, int n_seq,
                       int K, int32_t* accept_len, int32_t* next_anchor, int32_t* commit_offsets,
                       int32_t* commit_tokens, hdf_stream_t stream);
+
+/* Context growth after a round (Sec. 1: the n_s accepted drafts and the target's token
+ * after them join the context; Sec. 3.4: tau = n_s + 1): for every s,
+ *   ctx_len[s]    += accept_len[s] + 1
+ *   new_counts[s]  = accept_len[s] + 1          (skipped when new_counts is NULL)
+ * accept_len  [n_seq] int32 (device): hdf_accept's output
+ * ctx_len     [n_seq] int32 (device, in/out); new_counts [n_seq] int32 (device, out)
+ * The next round's hdf_draft_block_paged takes ctx_len and new_counts as they are,
+ * with no host read in between.  The caller keeps max_ctx and the page table ahead of
+ * the growth (at most B positions a round with B = K + 1). */
+hdf_status hdf_advance_context(int n_seq, const int32_t* accept_len, int32_t* ctx_len,
+                               int32_t* new_counts, hdf_stream_t stream);
 
 /* ------------------------------------------------------------------------------
  * 5. Temperature sampling and speculative-sampling verification (the temperature-1

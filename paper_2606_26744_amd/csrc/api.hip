@@ -450,7 +450,8 @@ size_t hdf_draft_block_workspace(const hdf_drafter* w, int n_seq, int B, int64_t
 // cache then holds kv_cap / 64 pages).
 static hdf_status draft_block_impl(const hdf_drafter* w, int n_seq, int B, const int32_t* ctx_len,
                                    int max_ctx, const void* y_new, const int32_t* new_offsets,
-                                   int64_t n_new, const int32_t* kv_offsets,
+                                   const int32_t* new_counts, int64_t n_new,
+                                   const int32_t* kv_offsets,
                                    const int32_t* page_table, int max_pages, void* kv_k,
                                    void* kv_vt, int64_t kv_cap, const int32_t* tokens,
                                    void* hidden, void* ws, size_t ws_bytes,
@@ -521,7 +522,8 @@ static hdf_status draft_block_impl(const hdf_drafter* w, int n_seq, int B, const
   auto prep = [&](int64_t r0, int rows, bool block) {
     hdf::PrepArgs pa{};
     pa.y = y_new; pa.r0 = r0; pa.n_ctx = rows; pa.ctx_gamma = w->ctx_norm; pa.c = cbuf;
-    pa.ctx_len = ctx_len; pa.new_offsets = new_offsets; pa.kv_offsets = kv_offsets;
+    pa.ctx_len = ctx_len; pa.new_offsets = new_offsets; pa.new_counts = new_counts;
+    pa.kv_offsets = kv_offsets;
     pa.page_table = page_table; pa.max_pages = max_pages;
     pa.n_seq = n_seq; pa.plan_pos = plan_pos; pa.plan_row = plan_row;
     pa.n_blk = block ? M : 0; pa.tokens = tokens; pa.emb = w->tok_emb;
@@ -646,13 +648,15 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
                            int64_t kv_cap, const int32_t* tokens, void* hidden, void* ws,
                            size_t ws_bytes, hdf_stream_t stream) {
   if (n_seq > 0 && kv_offsets == nullptr) return fail(HDF_E_INVALID, "draft_block: null kv_offsets");
-  return draft_block_impl(w, n_seq, B, ctx_len, max_ctx, y_new, new_offsets, n_new, kv_offsets,
-                          nullptr, 0, kv_k, kv_vt, kv_cap, tokens, hidden, ws, ws_bytes, stream);
+  return draft_block_impl(w, n_seq, B, ctx_len, max_ctx, y_new, new_offsets, nullptr, n_new,
+                          kv_offsets, nullptr, 0, kv_k, kv_vt, kv_cap, tokens, hidden, ws,
+                          ws_bytes, stream);
 }
 
 hdf_status hdf_draft_block_paged(const hdf_drafter* w, int n_seq, int B, const int32_t* ctx_len,
                                  int max_ctx, const void* y_new, const int32_t* new_offsets,
-                                 int64_t n_new, const int32_t* page_table, int max_pages,
+                                 const int32_t* new_counts, int64_t n_new,
+                                 const int32_t* page_table, int max_pages,
                                  void* kv_k, void* kv_vt, int64_t kv_pages,
                                  const int32_t* tokens, void* hidden, void* ws, size_t ws_bytes,
                                  hdf_stream_t stream) {
@@ -662,9 +666,20 @@ hdf_status hdf_draft_block_paged(const hdf_drafter* w, int n_seq, int B, const i
   if (kv_pages < 0 || kv_pages > INT32_MAX / 64)
     return fail(HDF_E_INVALID, "draft_block_paged: kv_pages=%lld outside [0, 2^25)",
                 static_cast<long long>(kv_pages));
-  return draft_block_impl(w, n_seq, B, ctx_len, max_ctx, y_new, new_offsets, n_new, nullptr,
-                          page_table, max_pages, kv_k, kv_vt, kv_pages * 64, tokens, hidden, ws,
-                          ws_bytes, stream);
+  return draft_block_impl(w, n_seq, B, ctx_len, max_ctx, y_new, new_offsets, new_counts, n_new,
+                          nullptr, page_table, max_pages, kv_k, kv_vt, kv_pages * 64, tokens,
+                          hidden, ws, ws_bytes, stream);
+}
+
+hdf_status hdf_advance_context(int n_seq, const int32_t* accept_len, int32_t* ctx_len,
+                               int32_t* new_counts, hdf_stream_t stream) {
+  if (n_seq < 0) return fail(HDF_E_INVALID, "advance_context: n_seq < 0");
+  if (n_seq > 0 && (accept_len == nullptr || ctx_len == nullptr))
+    return fail(HDF_E_INVALID, "advance_context: null accept_len/ctx_len");
+  const hipError_t e = hdf::launch_advance_context(n_seq, accept_len, ctx_len, new_counts,
+                                                   reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "advance_context launch");
+  return ok();
 }
 
 size_t hdf_packed_weight_bytes(int N, int K, hdf_dtype dtype) {

@@ -86,7 +86,7 @@ struct QkvEpiArgs {
   int first_part;        // 0: Q, K, V (block rows); 1: K, V only (context rows)
   int d, nh, hd, B;
   const int32_t* ctx_len;   // block rows: position = ctx_len[s] + k
-  const int32_t* plan_pos;  // context rows: position and cache row per row
+  const int32_t* plan_pos;  // context rows: position and cache row per row (-1: not a new row)
   const int32_t* plan_row;
   const float* rope_cs;     // [pos][hd/2][2] or NULL
   void* q;                  // block rows: [n_seq][nh][B][hd]
@@ -104,6 +104,7 @@ struct PrepArgs {
   void* c;
   const int32_t* ctx_len;
   const int32_t* new_offsets;
+  const int32_t* new_counts;   // [n_seq] rows of each sequence that are new, or NULL (all)
   const int32_t* kv_offsets;
   const int32_t* page_table;   // paged cache: [n_seq][max_pages] page of each 64-row tile, or NULL
   int max_pages;
@@ -121,6 +122,9 @@ struct PrepArgs {
   float eps;
 };
 hipError_t launch_prep(bool bf16, const PrepArgs& a, hipStream_t s);
+// ctx_len[s] += accept_len[s] + 1; new_counts[s] = accept_len[s] + 1 (new_counts may be NULL)
+hipError_t launch_advance_context(int n_seq, const int32_t* accept_len, int32_t* ctx_len,
+                                  int32_t* new_counts, hipStream_t s);
 // h += sum_z parts[z]; u = RMSNorm(h) * gamma
 hipError_t launch_residual_norm(bool bf16, const float* parts, int S, const float* gamma, float eps,
                                 int64_t rows, int d, float* h, void* u, hipStream_t s);

@@ -58,7 +58,10 @@ __device__ __forceinline__ float block_sum(float v, float* sh) {
 constexpr int kMaxGroups = 8;
 
 // First kernel of a drafter call, one 256-thread workgroup per row:
-//   context rows: (position, cache row) of the row, c = RMSNorm(y) * ctx_norm;
+//   context rows: (position, cache row) of the row, c = RMSNorm(y) * ctx_norm; a row past
+//                 its sequence's new rows (new_counts, or past new_offsets[n_seq]) or
+//                 outside the cached range gets position and cache row -1 and is not
+//                 stored by the epilogue;
 //   block rows:   h = float(emb[token]), u = RMSNorm(h) * attn_norm[0].
 template <typename T>
 __global__ void __launch_bounds__(kRowThreads)
@@ -77,10 +80,15 @@ prep_kernel(PrepArgs a) {
         const int mid = (lo + hi + 1) >> 1;
         if (a.new_offsets[mid] <= r) lo = mid; else hi = mid - 1;
       }
-      const int ns = a.new_offsets[lo + 1] - a.new_offsets[lo];
-      const int pos = a.ctx_len[lo] - ns + int(r - a.new_offsets[lo]);
-      a.plan_pos[r] = pos;
-      a.plan_row[r] = a.page_table != nullptr
+      int ns = a.new_offsets[lo + 1] - a.new_offsets[lo];
+      if (a.new_counts != nullptr) ns = min(ns, max(a.new_counts[lo], 0));
+      const int j = int(r - a.new_offsets[lo]);
+      const int pos = a.ctx_len[lo] - ns + j;
+      const bool valid = r < a.new_offsets[a.n_seq] && j < ns && pos >= 0 &&
+                         (a.page_table == nullptr || (pos >> 6) < a.max_pages);
+      a.plan_pos[r] = valid ? pos : -1;
+      a.plan_row[r] = !valid ? -1
+                      : a.page_table != nullptr
                           ? a.page_table[int64_t(lo) * a.max_pages + (pos >> 6)] * 64 + (pos & 63)
                           : a.kv_offsets[lo] + pos;
     }
@@ -215,6 +223,7 @@ qkv_epilogue_kernel(QkvEpiArgs a0, QkvEpiArgs a1, int nb0) {
   constexpr int QUADS = HALF / 4;
   for (int e = threadIdx.x; e < rows * nrot * QUADS; e += kRowThreads) {
     const int rr = e / (nrot * QUADS);
+    if (s_drow[rr] < 0) continue;   // a context row that is not new: nothing to store
     const int rem = e - rr * nrot * QUADS;
     const int pp = rem / QUADS;
     const int i0 = (rem - pp * QUADS) * 4;
@@ -273,7 +282,7 @@ qkv_epilogue_kernel(QkvEpiArgs a0, QkvEpiArgs a1, int nb0) {
   for (int e = threadIdx.x; e < rows * HD; e += kRowThreads) {
     const int i = e / rows;
     const int rr = e - i * rows;
-    store1<T>(vt + vc_index(s_drow[rr], i, HD), vt_tile[rr][i]);
+    if (s_drow[rr] >= 0) store1<T>(vt + vc_index(s_drow[rr], i, HD), vt_tile[rr][i]);
   }
 }
 
@@ -336,6 +345,26 @@ hipError_t launch_prep(bool bf16, const PrepArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(prep_kernel<bf16_t>, dim3(unsigned(wgs)), dim3(kRowThreads), 0, s, a);
   else
     hipLaunchKernelGGL(prep_kernel<float>, dim3(unsigned(wgs)), dim3(kRowThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+// After a verification round: sequence s committed accept_len[s] + 1 positions (its
+// accepted drafts and the target's token after them), which become its newest context
+// rows for the next round.
+__global__ void advance_context_kernel(int n_seq, const int32_t* __restrict__ accept_len,
+                                       int32_t* __restrict__ ctx_len, int32_t* __restrict__ new_counts) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= n_seq) return;
+  const int n = accept_len[s] + 1;
+  ctx_len[s] += n;
+  if (new_counts != nullptr) new_counts[s] = n;
+}
+
+hipError_t launch_advance_context(int n_seq, const int32_t* accept_len, int32_t* ctx_len,
+                                  int32_t* new_counts, hipStream_t s) {
+  if (n_seq <= 0) return hipSuccess;
+  hipLaunchKernelGGL(advance_context_kernel, dim3(unsigned((n_seq + 255) / 256)), dim3(256), 0, s,
+                     n_seq, accept_len, ctx_len, new_counts);
   return hipGetLastError();
 }
 

@@ -27,7 +27,8 @@ EXPORTS = ("hdf_last_error", "hdf_version", "hdf_hc_reduce", "hdf_rope_table",
            "hdf_draft_block_paged", "hdf_fc_reduce_workspace", "hdf_fc_reduce",
            "hdf_lm_head_workspace", "hdf_lm_head_argmax", "hdf_accept",
            "hdf_sample_workspace", "hdf_sample_tokens", "hdf_accept_sample_workspace",
-           "hdf_accept_sample", "hdf_kl_forward_workspace", "hdf_kl_forward")
+           "hdf_accept_sample", "hdf_kl_forward_workspace", "hdf_kl_forward",
+           "hdf_advance_context")
 
 
 class HdfError(RuntimeError):
@@ -89,8 +90,10 @@ def lib() -> ctypes.CDLL:
     L.hdf_draft_block.argtypes = [ctypes.POINTER(Drafter), _I, _I, _P, _I, _P, _P, _I64, _P, _P, _P,
                                   _I64, _P, _P, _P, _SZ, _P]
     L.hdf_draft_block_paged.restype = _I
-    L.hdf_draft_block_paged.argtypes = [ctypes.POINTER(Drafter), _I, _I, _P, _I, _P, _P, _I64, _P,
-                                        _I, _P, _P, _I64, _P, _P, _P, _SZ, _P]
+    L.hdf_draft_block_paged.argtypes = [ctypes.POINTER(Drafter), _I, _I, _P, _I, _P, _P, _P, _I64,
+                                        _P, _I, _P, _P, _I64, _P, _P, _P, _SZ, _P]
+    L.hdf_advance_context.restype = _I
+    L.hdf_advance_context.argtypes = [_I, _P, _P, _P, _P]
     L.hdf_fc_reduce_workspace.restype = _SZ
     L.hdf_fc_reduce_workspace.argtypes = [_I64, _I, _I, _I]
     L.hdf_fc_reduce.restype = _I
@@ -191,24 +194,42 @@ def fc_reduce(H: torch.Tensor, W_fc: "PackedWeight", b_fc: Optional[torch.Tensor
 # ----------------------------------------------------------------------------- accept
 
 def accept(draft: torch.Tensor, target: torch.Tensor, *, K: Optional[int] = None,
-           draft_stride: Optional[int] = None, commits: bool = True, stream=None):
+           draft_stride: Optional[int] = None, commits: bool = True, out=None, stream=None):
     """hdf_accept.  draft: int32 with row s at s*draft_stride (a [n_seq, >=K] tensor or a
-    view into a bigger array), target [n_seq, K+1] int32."""
+    view into a bigger array), target [n_seq, K+1] int32.  out: optional preallocated
+    (accept_len, next_anchor, commit_offsets, commit_tokens)."""
     n_seq = target.shape[0]
     K = target.shape[1] - 1 if K is None else K
     if draft_stride is None:
         draft_stride = draft.stride(0) if draft.dim() == 2 else K
     dev = target.device
-    acc = torch.empty(n_seq, dtype=torch.int32, device=dev)
-    anc = torch.empty(n_seq, dtype=torch.int32, device=dev)
-    offs = torch.empty(n_seq + 1, dtype=torch.int32, device=dev) if commits else None
-    toks = torch.empty(max(1, n_seq * (K + 1)), dtype=torch.int32, device=dev) if commits else None
-    _dev(target, acc)
+    if out is not None:
+        acc, anc, offs, toks = out
+    else:
+        acc = torch.empty(n_seq, dtype=torch.int32, device=dev)
+        anc = torch.empty(n_seq, dtype=torch.int32, device=dev)
+        offs = torch.empty(n_seq + 1, dtype=torch.int32, device=dev) if commits else None
+        toks = (torch.empty(max(1, n_seq * (K + 1)), dtype=torch.int32, device=dev)
+                if commits else None)
+    _dev(target, acc, anc, offs, toks)
     if not draft.is_cuda:
         raise ValueError("libhdf takes device tensors")
     _check(lib().hdf_accept(_ptr(draft), draft_stride, _ptr(target), n_seq, K, _ptr(acc),
                             _ptr(anc), _ptr(offs), _ptr(toks), _stream(stream)))
     return acc, anc, offs, toks
+
+
+def advance_context(accept_len: torch.Tensor, ctx_len: torch.Tensor,
+                    new_counts: Optional[torch.Tensor] = None, stream=None):
+    """hdf_advance_context: ctx_len += accept_len + 1 and new_counts = accept_len + 1, on
+    the device (int32 [n_seq] tensors; ctx_len in place)."""
+    n_seq = ctx_len.shape[0]
+    for t in (accept_len, ctx_len, new_counts):
+        if t is not None and (t.dtype != torch.int32 or t.numel() != n_seq):
+            raise ValueError("advance_context takes int32 [n_seq] tensors")
+    _dev(accept_len, ctx_len, new_counts)
+    _check(lib().hdf_advance_context(n_seq, _ptr(accept_len), _ptr(ctx_len), _ptr(new_counts),
+                                     _stream(stream)))
 
 
 # ----------------------------------------------------------------------------- sampling
@@ -419,12 +440,17 @@ class DrafterHandle:
                     new_offsets: torch.Tensor, kv_k: torch.Tensor, kv_vt: torch.Tensor,
                     tokens: torch.Tensor, kv_offsets: Optional[torch.Tensor] = None,
                     page_table: Optional[torch.Tensor] = None,
+                    new_counts: Optional[torch.Tensor] = None,
                     hidden: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
                     stream=None):
         """hdf_draft_block over a contiguous cache (kv_offsets [n_seq+1]) or
-        hdf_draft_block_paged over a paged one (page_table [n_seq][max_pages])."""
+        hdf_draft_block_paged over a paged one (page_table [n_seq][max_pages], optionally
+        with device new_counts [n_seq]: only the first new_counts[s] rows of each
+        sequence's rows in y_new are new)."""
         if (kv_offsets is None) == (page_table is None):
             raise ValueError("give exactly one of kv_offsets and page_table")
+        if new_counts is not None and page_table is None:
+            raise ValueError("new_counts goes with a paged cache")
         n_seq, B = tokens.shape
         n_new = y_new.shape[0]
         dev = tokens.device
@@ -437,10 +463,15 @@ class DrafterHandle:
             if page_table.dtype != torch.int32 or page_table.dim() != 2 or \
                     page_table.shape[0] != n_seq or not page_table.is_contiguous():
                 raise ValueError("page_table must be a contiguous int32 [n_seq][max_pages] tensor")
-            _dev(ctx_len, y_new, new_offsets, page_table, kv_k, kv_vt, tokens, hidden, ws)
+            if new_counts is not None and (new_counts.dtype != torch.int32 or
+                                           new_counts.numel() != n_seq):
+                raise ValueError("new_counts must be an int32 [n_seq] tensor")
+            _dev(ctx_len, y_new, new_offsets, new_counts, page_table, kv_k, kv_vt, tokens, hidden,
+                 ws)
             _check(lib().hdf_draft_block_paged(
                 ctypes.byref(self.s), n_seq, B, _ptr(ctx_len), max_ctx, _ptr(y_new),
-                _ptr(new_offsets), n_new, _ptr(page_table), page_table.shape[1], _ptr(kv_k),
+                _ptr(new_offsets), _ptr(new_counts), n_new, _ptr(page_table), page_table.shape[1],
+                _ptr(kv_k),
                 _ptr(kv_vt), kv_k.shape[2], _ptr(tokens), _ptr(hidden), _ptr(ws), ws.numel(),
                 _stream(stream)))
             return hidden

@@ -145,7 +145,7 @@ def test_draft_block_paged_validation():
 
     def call(page_table, max_pages, kv_pages, n_seq=2, max_ctx=100):
         return _status(L.hdf_draft_block_paged(ctypes.byref(w), n_seq, 16, fake, max_ctx, fake,
-                                               fake, 8, page_table, max_pages, fake, fake,
+                                               fake, None, 8, page_table, max_pages, fake, fake,
                                                kv_pages, fake, fake, fake, ws, None))
     assert call(None, 4, 8) == "HDF_E_INVALID"                 # no page table
     assert call(fake, 1, 8) == "HDF_E_INVALID"                 # 64 rows < max_ctx = 100
@@ -157,6 +157,16 @@ def test_draft_block_paged_validation():
     st = L.hdf_draft_block(ctypes.byref(w), 2, 16, fake, 100, fake, fake, 8, None, fake, fake,
                            128, fake, fake, fake, ws, None)
     assert _status(st) == "HDF_E_INVALID"
+
+
+def test_advance_context_validation():
+    """Null inputs and a negative count are rejected on the host; n_seq = 0 is a no-op."""
+    L = hdf.lib()
+    fake = ctypes.c_void_p(4096)
+    assert _status(L.hdf_advance_context(-1, fake, fake, fake, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_advance_context(2, None, fake, fake, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_advance_context(2, fake, None, None, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_advance_context(0, None, None, None, None)) == "HDF_OK"
 
 
 def test_fc_reduce_validation():
