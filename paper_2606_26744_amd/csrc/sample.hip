@@ -154,15 +154,39 @@ row_pass_kernel(const float* __restrict__ logits, int64_t ld, int V, int n_parts
     for (int q = 0; q < kGroupsPerPass; ++q) {
       const int g = g0 + q * kSampleThreads;
       if (8 * g >= c1) continue;
-      float u[8];
-      if constexpr (SAMPLE) uniforms8(seed, stream, uint64_t(row), uint64_t(g), kPurposeDraft, u);
+      const int nv = min(8, c1 - 8 * g);   // valid entries of the group (8 but at the end)
+      float xs[8];
+      float gm = -INFINITY;
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        const int v = 8 * g + k;
-        if (v < c1) {
-          const float xs = x[q][k] * inv_t;
-          lse_add(st, xs);
-          if constexpr (SAMPLE) best_add(st, xs + gumbel(u[k]), v);
+        xs[k] = k < nv ? x[q][k] * inv_t : -INFINITY;
+        gm = fmaxf(gm, xs[k]);
+      }
+      // One rescale per group: s <- s e^(m - m') + sum_k e^(x_k - m'), m' = max(m, max_k x_k).
+      const float mn = fmaxf(st.m, gm);
+      float add = 0.f;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) add += __expf(xs[k] - mn);
+      st.s = st.s * __expf(st.m - mn) + add;
+      st.m = mn;
+      if constexpr (SAMPLE) {
+        float u[8];
+        uniforms8(seed, stream, uint64_t(row), uint64_t(g), kPurposeDraft, u);
+        // The group's best perturbed score, lowest index first; groups come in increasing
+        // order, so a tie with the running best keeps the running (lower) index.
+        float gb = -INFINITY;
+        int gk = 0;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const float sc = k < nv ? xs[k] - __logf(-logf(u[k])) : -INFINITY;
+          if (sc > gb) {
+            gb = sc;
+            gk = k;
+          }
+        }
+        if (gb > st.best) {
+          st.best = gb;
+          st.idx = 8 * g + gk;
         }
       }
     }
