@@ -569,8 +569,17 @@ static hdf_status draft_block_impl(const hdf_drafter* w, int n_seq, int B, const
       // Rows d..3d-1 (W_k; W_v) of the packed W_qkv: d/128 whole row groups in.
       const char* wkv = static_cast<const char*>(w->w_qkv[l]) + size_t(d) * d * el;
       const hdf::GemmPlan Sp = hdf::gemm_plan(bf, rows, 2 * d, d);
-      HDF_TRY(hdf::launch_gemm_partial(bf, cbuf, d, wkv, rows, 2 * d, d, Sp, parts, s));
-      HDF_TRY(hdf::launch_qkv_epilogue(bf, ctx_epi(l, r0, rows, Sp.splits, parts), s));
+      if (bf && Sp.tn == 2 && Sp.nw == 8 && Sp.splits == 1 && (hd == 64 || hd == 128) &&
+          d % 512 == 0) {
+        // One K split: RoPE and the cache stores happen in the GEMM's epilogue, so the
+        // fp32 rows never go through memory.
+        HDF_TRY(hdf::launch_gemm_kv(cbuf, d, wkv, rows, d, hd, Sp, plan_pos + r0, plan_row + r0,
+                                    w->rope_cs, static_cast<char*>(kv_k) + l * layer_kv,
+                                    static_cast<char*>(kv_vt) + l * layer_kv, kv_cap, s));
+      } else {
+        HDF_TRY(hdf::launch_gemm_partial(bf, cbuf, d, wkv, rows, 2 * d, d, Sp, parts, s));
+        HDF_TRY(hdf::launch_qkv_epilogue(bf, ctx_epi(l, r0, rows, Sp.splits, parts), s));
+      }
     }
   }
 

@@ -75,12 +75,12 @@ gemm_bf16_kernel(GemmArgs p) {
   constexpr int A_CHUNKS = BM * kBK / 8;           // 16-byte chunks of an activation step
   constexpr int A_CH = (A_CHUNKS + THREADS - 1) / THREADS;
   constexpr int LDC = 33;                         // padded row of a wave's 32 columns
-  static_assert(EPI != kEpiArgmax || NB % 4 == 0, "argmax tiles are whole 128-column slabs");
+  static_assert(EPI == kEpiPartial || NB % 4 == 0, "argmax and K/V tiles are whole 128-column slabs");
   // LDS: the double-buffered activation tile, reused after the K loop by the ARGMAX
   // epilogue to stage the fp32 tile of four waves at a time ([wave][row][32 columns]).
   constexpr size_t kMainLds = PP ? size_t(4) * BM * (32 + 8) * sizeof(bf16_t)   // NBUF units
                                 : size_t(2) * BM * LDA * sizeof(bf16_t);
-  constexpr size_t kEpiLds = (EPI == kEpiArgmax) ? size_t(4) * BM * LDC * sizeof(float) : 0;
+  constexpr size_t kEpiLds = (EPI != kEpiPartial) ? size_t(4) * BM * LDC * sizeof(float) : 0;
   __shared__ __attribute__((aligned(16))) unsigned char smem[kMainLds > kEpiLds ? kMainLds : kEpiLds];
   typedef bf16_t ATile[BM][LDA];
   ATile* As = reinterpret_cast<ATile*>(smem);
@@ -309,6 +309,102 @@ gemm_bf16_kernel(GemmArgs p) {
           const int row = m0 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
           if (row < p.M && col < p.N) C[int64_t(row) * p.N + col] = acc[i][tn][r];
         }
+    }
+  } else if constexpr (EPI == kEpiKV) {
+    // Context K/V rows straight into the cache, one 128-column slab (whole heads) of the
+    // tile at a time through LDS ([block][row][column of the block]): K columns get RoPE
+    // at the row's position (pairs i, i + hd/2 of a head) and go to the key tile layout,
+    // four consecutive dims per store; V columns go to the transposed value layout with
+    // consecutive threads on consecutive rows of one dim.  The same fp32 values and the
+    // same rounding as the partial-sum path and its epilogue kernel.
+    float* Cs = reinterpret_cast<float*>(smem);
+    const bool is_v = n0 >= p.kv_d;
+    const int HD = p.hd, HALF = HD >> 1;
+    auto at = [&](int rr, int cc) { return Cs[((cc >> 5) * BM + rr) * LDC + (cc & 31)]; };
+#pragma unroll 1
+    for (int slab = 0; slab < NB / 4; ++slab) {
+      if (slab > 0) __syncthreads();
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        const int b = wid * TN + tn;
+        if ((b >> 2) == slab) {
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int rr = 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+              Cs[((b & 3) * BM + rr) * LDC + (lane & 31)] = acc[i][tn][r];
+            }
+        }
+      }
+      __syncthreads();
+      const int c0 = n0 + 128 * slab - (is_v ? p.kv_d : 0);   // slab start inside K or V
+      if (c0 >= p.kv_d) continue;                             // columns past N
+      if (!is_v) {
+        // Items (row, octet of eight rotated pairs): 8 octets per row of the slab, each
+        // stored as two 16-byte runs (dims i0..i0+7 and i0+hd/2..i0+hd/2+7 are contiguous
+        // in the key tile layout).
+        for (int e = tid; e < BM * 8; e += THREADS) {
+          const int rr = e >> 3, oc = e & 7;
+          const int row = m0 + rr;
+          if (row >= p.M) continue;
+          const int drow = p.plan_row[row];
+          if (drow < 0) continue;
+          const int j = (8 * oc) / HALF;        // head inside the slab
+          const int i0 = 8 * oc - j * HALF;
+          float y1[8], y2[8];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) {
+            y1[k] = at(rr, j * HD + i0 + k);
+            y2[k] = at(rr, j * HD + HALF + i0 + k);
+          }
+          if (p.rope_cs != nullptr) {
+            const float* cs = p.rope_cs + (int64_t(p.plan_pos[row]) * HALF + i0) * 2;
+#pragma unroll
+            for (int k = 0; k < 8; k += 2) {
+              const float4 c = *reinterpret_cast<const float4*>(cs + 2 * k);
+              rope_rotate(y1[k], y2[k], c.x, c.y);
+              rope_rotate(y1[k + 1], y2[k + 1], c.z, c.w);
+            }
+          }
+          bf16_t* kh = static_cast<bf16_t*>(p.kc) + int64_t(c0 / HD + j) * p.cap * HD;
+          *reinterpret_cast<uint4*>(kh + kc_index(drow, i0, HD)) =
+              make_uint4(pack_bf2(y1[0], y1[1]), pack_bf2(y1[2], y1[3]), pack_bf2(y1[4], y1[5]),
+                         pack_bf2(y1[6], y1[7]));
+          *reinterpret_cast<uint4*>(kh + kc_index(drow, i0 + HALF, HD)) =
+              make_uint4(pack_bf2(y2[0], y2[1]), pack_bf2(y2[2], y2[3]), pack_bf2(y2[4], y2[5]),
+                         pack_bf2(y2[6], y2[7]));
+        }
+      } else {
+        // Items (group of 8 rows, dim): consecutive threads on consecutive dims; a group
+        // whose 8 rows are 8 consecutive cache rows starting at a multiple of 8 is one
+        // 16-byte run of the value tile layout, any other group is stored element-wise.
+        for (int e = tid; e < (BM / 8) * 128; e += THREADS) {
+          const int cc = e & 127, rg = e >> 7;
+          const int row0 = m0 + 8 * rg;
+          if (row0 >= p.M) continue;
+          const int col = c0 + cc;
+          bf16_t* vh = static_cast<bf16_t*>(p.vtc) + int64_t(col / HD) * p.cap * HD;
+          const int i = col % HD;
+          const int d0 = p.plan_row[row0];
+          bool run = row0 + 8 <= p.M && d0 >= 0 && (d0 & 7) == 0;
+#pragma unroll
+          for (int k = 1; k < 8; ++k) run = run && p.plan_row[row0 + k] == d0 + k;
+          if (run) {
+            float v[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) v[k] = at(8 * rg + k, cc);
+            *reinterpret_cast<uint4*>(vh + vc_index(d0, i, HD)) =
+                make_uint4(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]),
+                           pack_bf2(v[6], v[7]));
+          } else {
+            for (int k = 0; k < 8 && row0 + k < p.M; ++k) {
+              const int dr = p.plan_row[row0 + k];
+              if (dr >= 0) vh[vc_index(dr, i, HD)] = f2bf(at(8 * rg + k, cc));
+            }
+          }
+        }
+      }
     }
   } else {
     // Stage the fp32 tile in LDS, four waves (128 columns) at a time ([wave][row][column
@@ -676,6 +772,25 @@ hipError_t launch_gemm_partial2(const void* A, int64_t lda, const void* B, int M
   a.M = M; a.N = N; a.K = K; a.C = C; a.keys = nullptr;
   a.A2 = A2; a.lda2 = lda2; a.B2 = B2; a.M2 = M2; a.N2 = N2; a.C2 = C2;
   return launch_gemm_any(true, kEpiPartial, a, plan, s);
+}
+
+hipError_t launch_gemm_kv(const void* A, int64_t lda, const void* B, int M, int d, int hd,
+                          GemmPlan plan, const int32_t* plan_pos, const int32_t* plan_row,
+                          const float* rope_cs, void* kc, void* vtc, int64_t cap, hipStream_t s) {
+  // 512-column tiles lie wholly in K or in V when d % 512 == 0.
+  if (plan.tn != 2 || plan.nw != 8 || plan.splits != 1 || (hd != 64 && hd != 128) ||
+      d % 512 != 0)
+    return hipErrorInvalidValue;
+  if (M <= 0) return hipSuccess;
+  GemmArgs a{};
+  a.A = A; a.lda = lda; a.B = B;
+  a.M = M; a.N = 2 * d; a.K = d;
+  a.plan_pos = plan_pos; a.plan_row = plan_row; a.rope_cs = rope_cs;
+  a.kc = kc; a.vtc = vtc; a.cap = cap; a.kv_d = d; a.hd = hd;
+  const int tiles = ((M + 127) / 128) * ((2 * d + 511) / 512);
+  hipLaunchKernelGGL((gemm_bf16_kernel<128, 8, 2, kEpiKV, 2, false, true>), dim3(tiles), dim3(512),
+                     0, s, a);
+  return hipGetLastError();
 }
 
 GemmPlan lm_head_plan(int64_t) {

@@ -27,6 +27,7 @@ hipError_t launch_accept(const int32_t* draft, int stride, const int32_t* target
 // ---------------------------------------------------------------- GEMM (gemm.hip)
 constexpr int kEpiPartial = 0;  // fp32 C / split-K partials
 constexpr int kEpiArgmax = 1;   // LM head: fused row argmax (+ optional fp32 logits in C)
+constexpr int kEpiKV = 2;       // context K/V rows: RoPE on K, stored into the cache layouts
 
 struct GemmArgs {
   const void* A;   // [M][lda] row-major activations
@@ -42,6 +43,15 @@ struct GemmArgs {
   const void* B2;
   int M2, N2;
   float* C2;
+  // kEpiKV: columns [0, kv_d) are K, [kv_d, 2 kv_d) V, in heads of hd; row r goes to
+  // cache row plan_row[r] (-1: not stored) at position plan_pos[r].
+  const int32_t* plan_pos;
+  const int32_t* plan_row;
+  const float* rope_cs;   // [pos][hd/2][2] or NULL
+  void* kc;               // [nh][cap][hd] key tiles of the layer
+  void* vtc;              // [nh][hd][cap] value tiles of the layer
+  int64_t cap;
+  int kv_d, hd;
 };
 
 int gemm_k_align(bool bf16);                       // K must be a multiple of this
@@ -67,6 +77,13 @@ hipError_t launch_gemm_partial(bool bf16, const void* A, int64_t lda, const void
 hipError_t launch_gemm_partial2(const void* A, int64_t lda, const void* B, int M, int N,
                                 float* C, const void* A2, int64_t lda2, const void* B2, int M2,
                                 int N2, float* C2, int K, GemmPlan plan, hipStream_t s);
+// Context K/V projection straight into the cache: A [M][d] normed context rows (bf16),
+// B the packed W_k; W_v rows (2d x d), RoPE on K at plan_pos, stores at plan_row.  Only
+// for plans of one K split and two-block waves and d % 512 == 0 (returns
+// hipErrorInvalidValue otherwise).
+hipError_t launch_gemm_kv(const void* A, int64_t lda, const void* B, int M, int d, int hd,
+                          GemmPlan plan, const int32_t* plan_pos, const int32_t* plan_row,
+                          const float* rope_cs, void* kc, void* vtc, int64_t cap, hipStream_t s);
 // keys: M 64-bit scratch words.  logits may be NULL.
 hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t M, int d, int V,
                           unsigned long long* keys, int32_t* argmax, float* max_logit,

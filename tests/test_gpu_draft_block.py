@@ -142,6 +142,16 @@ def test_ragged_long_contexts_sampled():
     torch.cuda.empty_cache()
 
 
+def test_cold_rows_projected_into_the_cache_by_the_gemm_epilogue():
+    """8192 cold context rows at head_dim 64 over a paged pool: one K split, so RoPE and
+    the cache stores happen in the projection GEMM's epilogue (no fp32 rows in memory)."""
+    wl = synth.small_bf16()
+    case = DraftCase(wl, [4096, 4096], [4096, 4096], sub=15, paged=True, spare_pages=3)
+    _compare(case, seqs=[1])
+    del case
+    torch.cuda.empty_cache()
+
+
 def test_paged_cache_scattered_pages():
     """Paged cache: every sequence's 64-row tiles sit at random pages of a shared pool
     (with spare pages in between); warm and cold rows, ragged lengths, one and two
