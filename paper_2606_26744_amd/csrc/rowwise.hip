@@ -54,9 +54,6 @@ __device__ __forceinline__ float block_sum(float v, float* sh) {
   return t;
 }
 
-// Rows are at most 8192 wide: 8 groups of 4 per thread at 256 threads.
-constexpr int kMaxGroups = 8;
-
 // First kernel of a drafter call, one 256-thread workgroup per row:
 //   context rows: (position, cache row) of the row, c = RMSNorm(y) * ctx_norm; a row past
 //                 its sequence's new rows (new_counts, or past new_offsets[n_seq]) or
@@ -64,67 +61,98 @@ constexpr int kMaxGroups = 8;
 //                 stored by the epilogue;
 //   block rows:   h = float(emb[token]), u = RMSNorm(h) * attn_norm[0].
 template <typename T>
+__device__ __forceinline__ void load8(const T* p, float* v);
+template <>
+__device__ __forceinline__ void load8<bf16_t>(const bf16_t* p, float* v) {
+  const uint4 u = *reinterpret_cast<const uint4*>(p);
+  v[0] = lo_bf(u.x); v[1] = hi_bf(u.x); v[2] = lo_bf(u.y); v[3] = hi_bf(u.y);
+  v[4] = lo_bf(u.z); v[5] = hi_bf(u.z); v[6] = lo_bf(u.w); v[7] = hi_bf(u.w);
+}
+template <>
+__device__ __forceinline__ void load8<float>(const float* p, float* v) {
+  load4<float>(p, v);
+  load4<float>(p + 4, v + 4);
+}
+template <typename T>
+__device__ __forceinline__ void store8(T* p, const float* v);
+template <>
+__device__ __forceinline__ void store8<bf16_t>(bf16_t* p, const float* v) {
+  *reinterpret_cast<uint4*>(p) = make_uint4(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]),
+                                            pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7]));
+}
+template <>
+__device__ __forceinline__ void store8<float>(float* p, const float* v) {
+  store4<float>(p, v);
+  store4<float>(p + 4, v + 4);
+}
+
+// Eight consecutive elements per thread and group: rows up to 4 x 8 x 256 = 8192 wide.
+constexpr int kMaxGroups8 = 4;
+
+template <typename T>
 __global__ void __launch_bounds__(kRowThreads)
 prep_kernel(PrepArgs a) {
   __shared__ float sh[kRowThreads / 64];
   const int b = blockIdx.x;
-  const T* x;
-  float* hrow = nullptr;
-  const float* gamma;
-  T* out;
-  if (b < a.n_ctx) {
-    const int64_t r = a.r0 + b;
-    if (threadIdx.x == 0) {
-      int lo = 0, hi = a.n_seq - 1;   // last s with new_offsets[s] <= r
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (a.new_offsets[mid] <= r) lo = mid; else hi = mid - 1;
-      }
-      int ns = a.new_offsets[lo + 1] - a.new_offsets[lo];
-      if (a.new_counts != nullptr) ns = min(ns, max(a.new_counts[lo], 0));
-      const int j = int(r - a.new_offsets[lo]);
-      const int pos = a.ctx_len[lo] - ns + j;
-      const bool valid = r < a.new_offsets[a.n_seq] && j < ns && pos >= 0 &&
-                         (a.page_table == nullptr || (pos >> 6) < a.max_pages);
-      a.plan_pos[r] = valid ? pos : -1;
-      a.plan_row[r] = !valid ? -1
-                      : a.page_table != nullptr
-                          ? a.page_table[int64_t(lo) * a.max_pages + (pos >> 6)] * 64 + (pos & 63)
-                          : a.kv_offsets[lo] + pos;
-    }
-    x = static_cast<const T*>(a.y) + r * a.d;
-    gamma = a.ctx_gamma;
-    out = static_cast<T*>(a.c) + int64_t(b) * a.d;
-  } else {
-    const int64_t r = b - a.n_ctx;
-    x = static_cast<const T*>(a.emb) + int64_t(a.tokens[r]) * a.d;
-    hrow = a.h + r * a.d;
-    gamma = a.attn_gamma;
-    out = static_cast<T*>(a.u) + r * a.d;
+  const bool ctx = b < a.n_ctx;
+  const int64_t r = ctx ? a.r0 + b : int64_t(b - a.n_ctx);
+  const T* x = ctx ? static_cast<const T*>(a.y) + r * a.d
+                   : static_cast<const T*>(a.emb) + int64_t(a.tokens[r]) * a.d;
+  // The row's loads first, so that the plan's dependent loads below overlap them.
+  float v[kMaxGroups8][8];
+#pragma unroll
+  for (int g = 0; g < kMaxGroups8; ++g) {
+    const int c = (g * kRowThreads + threadIdx.x) * 8;
+    if (c < a.d) load8<T>(x + c, v[g]);
   }
-  float v[kMaxGroups][4];
+  if (ctx && threadIdx.x == 0) {
+    int lo = 0, hi = a.n_seq - 1;   // last s with new_offsets[s] <= r
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (a.new_offsets[mid] <= r) lo = mid; else hi = mid - 1;
+    }
+    int ns = a.new_offsets[lo + 1] - a.new_offsets[lo];
+    if (a.new_counts != nullptr) ns = min(ns, max(a.new_counts[lo], 0));
+    const int j = int(r - a.new_offsets[lo]);
+    const int pos = a.ctx_len[lo] - ns + j;
+    const bool valid = r < a.new_offsets[a.n_seq] && j < ns && pos >= 0 &&
+                       (a.page_table == nullptr || (pos >> 6) < a.max_pages);
+    a.plan_pos[r] = valid ? pos : -1;
+    a.plan_row[r] = !valid ? -1
+                    : a.page_table != nullptr
+                        ? a.page_table[int64_t(lo) * a.max_pages + (pos >> 6)] * 64 + (pos & 63)
+                        : a.kv_offsets[lo] + pos;
+  }
+  float* hrow = ctx ? nullptr : a.h + r * a.d;
+  const float* gamma = ctx ? a.ctx_gamma : a.attn_gamma;
+  T* out = ctx ? static_cast<T*>(a.c) + int64_t(b) * a.d : static_cast<T*>(a.u) + r * a.d;
   float ss = 0.f;
 #pragma unroll
-  for (int g = 0; g < kMaxGroups; ++g) {
-    const int c = (g * kRowThreads + threadIdx.x) * 4;
+  for (int g = 0; g < kMaxGroups8; ++g) {
+    const int c = (g * kRowThreads + threadIdx.x) * 8;
     if (c < a.d) {
-      load4<T>(x + c, v[g]);
-      if (hrow != nullptr)
-        *reinterpret_cast<float4*>(hrow + c) = make_float4(v[g][0], v[g][1], v[g][2], v[g][3]);
+      if (hrow != nullptr) store8<float>(hrow + c, v[g]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) ss = fmaf(v[g][j], v[g][j], ss);
+      for (int j = 0; j < 8; ++j) ss = fmaf(v[g][j], v[g][j], ss);
     }
   }
   ss = block_sum(ss, sh);
   const float rs = rsqrtf(ss / float(a.d) + a.eps);
 #pragma unroll
-  for (int g = 0; g < kMaxGroups; ++g) {
-    const int c = (g * kRowThreads + threadIdx.x) * 4;
+  for (int g = 0; g < kMaxGroups8; ++g) {
+    const int c = (g * kRowThreads + threadIdx.x) * 8;
     if (c < a.d) {
-      float o[4];
+      float gm[8];
+      if (gamma != nullptr) {
+        load8<float>(gamma + c, gm);
+      } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) o[j] = v[g][j] * rs * (gamma ? gamma[c + j] : 1.f);
-      store4<T>(out + c, o);
+        for (int j = 0; j < 8; ++j) gm[j] = 1.f;
+      }
+      float o[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) o[j] = v[g][j] * rs * gm[j];
+      store8<T>(out + c, o);
     }
   }
 }
