@@ -100,7 +100,7 @@ hdf_status validate_drafter(const hdf_drafter* w) {
 
 struct DraftPlan {
   size_t plan_pos, plan_row, c, h, u, q, kb, vtb, parts, part_o, part_ml, attn, act, total;
-  int chunk_len, attn_waves;
+  int chunk_len;
 };
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
@@ -113,13 +113,14 @@ DraftPlan plan_workspace(const hdf_drafter& w, int n_seq, int B, int64_t n_new, 
   const size_t M = size_t(n_seq) * B;
   const size_t QB = size_t((B + 15) / 16) * 16;
   const int64_t crow = n_new < kCtxChunk ? n_new : kCtxChunk;
-  // Attention split.  When one round of 8-wave workgroups (one per CU) covers every
+  // Attention split (8-wave workgroups, one per CU).  When one round of them covers every
   // (sequence, head) pair, a chunk is the longest power of two from 512 up that still
   // gives every CU a workgroup (at most 16384): 8 x 2048 positions take one chunk of
-  // 2048 keys and need no merge.  Otherwise 4-wave workgroups take chunks of the longest power of two in
-  // [512, 4096] that still gives four workgroups per CU (each chunk costs a partial
-  // output and a merge): 4096 keys for 64 sequences of up to 16K positions (ragged step
-  // 3.82 -> 3.27 ms against 512).
+  // 2048 keys and need no merge.  Otherwise chunks are the longest power of two in
+  // [512, 8192] that still gives four workgroups per CU (each chunk costs a partial
+  // output and a merge): 8192 keys for 64 sequences of up to 16K positions (ragged step
+  // 3.82 -> 3.27 ms from 512 to 4096 keys with 4-wave workgroups, 3.22 -> 3.17 ms from
+  // those to 8-wave workgroups of 8192 keys).
   {
     const int64_t pairs = int64_t(n_seq) * w.n_heads * ((B + 15) / 16);
     const int64_t cus = hdf::device_cu_count();
@@ -127,16 +128,12 @@ DraftPlan plan_workspace(const hdf_drafter& w, int n_seq, int B, int64_t n_new, 
     while (c < hdf::kAttnMaxChunk && c < max_ctx &&
            pairs * ((max_ctx + 2 * c - 1) / (2 * c)) >= cus)
       c *= 2;
-    if (pairs * std::max<int64_t>(1, (max_ctx + c - 1) / c) <= cus) {
-      P.chunk_len = int(c);
-      P.attn_waves = 8;
-    } else {
+    if (pairs * std::max<int64_t>(1, (max_ctx + c - 1) / c) > cus) {
       const int64_t per_wg = int64_t(n_seq) * max_ctx * w.n_heads / (int64_t(4) * cus);
       c = 512;
-      while (c < 4096 && 2 * c <= per_wg) c *= 2;
-      P.chunk_len = int(c);
-      P.attn_waves = 4;
+      while (c < 8192 && 2 * c <= per_wg) c *= 2;
     }
+    P.chunk_len = int(c);
   }
   const size_t n_chunks = size_t(std::max(1, (max_ctx + P.chunk_len - 1) / P.chunk_len));
   size_t parts = 0;
@@ -624,7 +621,7 @@ static hdf_status draft_block_impl(const hdf_drafter* w, int n_seq, int B, const
     aa.page_table = page_table; aa.max_pages = max_pages;
     aa.kb = kb; aa.vtb = vtb; aa.capb = capb;
     aa.n_seq = n_seq; aa.nh = nh; aa.hd = hd; aa.B = B; aa.QB = ((B + 15) / 16) * 16;
-    aa.n_chunks = n_chunks; aa.chunk_len = P.chunk_len; aa.waves = P.attn_waves;
+    aa.n_chunks = n_chunks; aa.chunk_len = P.chunk_len;
     aa.scale_log2 = float(1.4426950408889634 / sqrt(double(hd)));
     aa.part_o = part_o; aa.part_ml = part_ml;
     HDF_TRY(hdf::launch_attention(bf, aa, attn, s));

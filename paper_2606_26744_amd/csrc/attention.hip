@@ -12,7 +12,7 @@
 // page page_table[s][j]; its block keys sit in 64-row slot s of separate block buffers
 // of the same layout.
 //
-// bf16 kernel: grid (chunk, head, sequence x 16-query group), NW = 4 or 8 waves.
+// bf16 kernel: grid (chunk, head, sequence x 16-query group), 8 waves.
 // With one chunk (n_chunks == 1) a workgroup takes all of its sequence's context
 // tiles and the block's tile and writes the normalised output rows.  Otherwise
 // chunks 0 .. n_chunks-1 take chunk_len context keys each and chunk n_chunks the
@@ -44,12 +44,13 @@ __device__ __forceinline__ int attn_ctx_chunks(const AttnArgs& a, int T) {
   return min(a.n_chunks, (T + a.chunk_len - 1) / a.chunk_len);
 }
 
-// Two waves per SIMD: 256 VGPRs per wave at most.
-template <int HD, int NW>
-__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)))
+constexpr int kAttnWaves = 8;
+constexpr int kAttnThreads = 64 * kAttnWaves;
+
+// Two waves per SIMD (one workgroup per CU): 256 VGPRs per wave at most.
+template <int HD>
+__global__ void __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)))
 attn_bf16_kernel(AttnArgs a, bf16_t* __restrict__ out) {
-  constexpr int kAttnWaves = NW;
-  constexpr int kAttnThreads = 64 * NW;
   constexpr int NJ = HD / 32;   // MFMA steps over the head dimension for S
   constexpr int NDT = HD / 16;  // 16-row tiles of O^T
   __shared__ float red_o[kAttnWaves][16][HD + 1];
@@ -403,20 +404,15 @@ hipError_t launch_attention(bool bf16, const AttnArgs& a, void* out, hipStream_t
                          static_cast<float*>(out));
     return hipGetLastError();
   }
-  if (a.n_chunks < 1 || a.chunk_len % kKeyTile != 0 || a.chunk_len > kAttnMaxChunk ||
-      (a.waves != 4 && a.waves != 8))
+  if (a.n_chunks < 1 || a.chunk_len % kKeyTile != 0 || a.chunk_len > kAttnMaxChunk)
     return hipErrorInvalidValue;
   const int nqg = (a.B + 15) / 16;
   const dim3 grid(a.n_chunks == 1 ? 1 : a.n_chunks + 1, a.nh, a.n_seq * nqg);
   bf16_t* o = static_cast<bf16_t*>(out);
-  const bool w8 = a.waves == 8;
-  if (a.hd == 128) {
-    if (w8) hipLaunchKernelGGL((attn_bf16_kernel<128, 8>), grid, dim3(512), 0, s, a, o);
-    else hipLaunchKernelGGL((attn_bf16_kernel<128, 4>), grid, dim3(256), 0, s, a, o);
-  } else {
-    if (w8) hipLaunchKernelGGL((attn_bf16_kernel<64, 8>), grid, dim3(512), 0, s, a, o);
-    else hipLaunchKernelGGL((attn_bf16_kernel<64, 4>), grid, dim3(256), 0, s, a, o);
-  }
+  if (a.hd == 128)
+    hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(kAttnThreads), 0, s, a, o);
+  else
+    hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(kAttnThreads), 0, s, a, o);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_chunks == 1) return e;
   const size_t lds = size_t(2) * 16 * (a.n_chunks + 1) * sizeof(float);

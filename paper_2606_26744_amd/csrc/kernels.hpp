@@ -194,7 +194,6 @@ struct AttnArgs {
   int64_t capb;
   int n_seq, nh, hd, B, QB;  // QB = B rounded up to 16
   int n_chunks, chunk_len;   // context chunks of the grid (chunk_len % 64 == 0)
-  int waves;                 // waves per workgroup of the bf16 kernel (4 or 8)
   float scale_log2;          // log2(e) / sqrt(hd)
   float* part_o;             // [n_seq][nh][n_chunks+1][QB][hd]
   float* part_ml;            // [n_seq][nh][n_chunks+1][QB][2]

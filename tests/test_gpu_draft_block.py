@@ -81,11 +81,10 @@ def test_head_dim_128_and_loose_max_ctx():
     _compare(DraftCase(wl, [300, 1500, 64], [20, 1500, 64], sub=4, max_ctx=3000))
 
 
-def test_many_sequences_four_wave_attention():
-    """More (sequence, head) pairs than the 256 CUs: the attention runs as 4-wave
-    workgroups, in several chunks per sequence merged by the combine kernel (contexts up
-    to 1100), then in one chunk per sequence written directly (contexts up to 500, one
-    of them empty)."""
+def test_many_sequences_attention_chunks():
+    """More (sequence, head) pairs than the 256 CUs: the attention takes several chunks
+    per sequence merged by the combine kernel (contexts up to 1100), then one chunk per
+    sequence written directly (contexts up to 500, one of them empty)."""
     wl = synth.small_bf16()
     rng = np.random.default_rng(17)
     ctx = [int(x) for x in rng.integers(1, 1100, size=20)]
@@ -95,7 +94,7 @@ def test_many_sequences_four_wave_attention():
     _compare(DraftCase(wl, ctx, [min(c, 16) for c in ctx], sub=13), seqs=[3, 5, 11])
 
 
-def test_many_sequences_four_wave_attention_head_dim_128():
+def test_many_sequences_attention_chunks_head_dim_128():
     wl = synth.small_bf16()
     wl.drafter = synth.DrafterShape(d=1024, n_layers=1, n_heads=8, head_dim=128, d_ff=2048,
                                     vocab=1000)
