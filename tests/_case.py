@@ -16,10 +16,12 @@ def bits(t):
 
 class DraftCase:
     """ctx[s] context length of sequence s; new[s] rows of it projected by this call (the
-    last ones); the rows before come from a synthetic already-filled cache."""
+    last ones); the rows before come from a synthetic already-filled cache.  With
+    `stride` (paged cache only) every sequence has `stride` rows in y_new of which the
+    first new[s] are new, given to the call as device row counts."""
 
     def __init__(self, wl, ctx, new, *, B=None, random_norms=True, rope=True, sub=0,
-                 max_ctx=None, y_from=None, paged=False, spare_pages=0):
+                 max_ctx=None, y_from=None, paged=False, spare_pages=0, stride=None):
         self.wl = wl = dataclasses.replace(wl, n_seq=len(ctx), ctx_lens=list(ctx),
                                            block=B or wl.block)
         dr = wl.drafter
@@ -75,9 +77,17 @@ class DraftCase:
                 else:
                     per_layer.append((np.zeros((0, dr.d)), np.zeros((0, dr.d))))
             self.prefix.append(per_layer)
-        no = [0]
-        for n in self.new:
-            no.append(no[-1] + n)
+        self.stride = stride
+        self.new_counts = None
+        if stride is not None:
+            if not paged or max(self.new) > stride:
+                raise ValueError("stride goes with a paged cache and new[s] <= stride")
+            no = [s_ * stride for s_ in range(len(self.ctx) + 1)]
+            self.new_counts = torch.tensor(self.new, dtype=torch.int32, device=dev)
+        else:
+            no = [0]
+            for n in self.new:
+                no.append(no[-1] + n)
         self.new_offsets = torch.tensor(no, dtype=torch.int32, device=dev)
         self.n_new = no[-1]
         self.y_new = (synth.reduced_states(wl, self.n_new, device=dev, sub=sub) if y_from is None
@@ -87,7 +97,8 @@ class DraftCase:
     def run(self, hidden=None, ws=None):
         return self.h.draft_block(ctx_len=self.ctx_len, max_ctx=self.max_ctx, y_new=self.y_new,
                                   new_offsets=self.new_offsets, kv_offsets=self.kv_offsets,
-                                  page_table=self.page_table, kv_k=self.kv_k, kv_vt=self.kv_vt,
+                                  page_table=self.page_table, new_counts=self.new_counts,
+                                  kv_k=self.kv_k, kv_vt=self.kv_vt,
                                   tokens=self.tokens, hidden=hidden, ws=ws)
 
     def read_cache(self, s, layer):
@@ -107,7 +118,7 @@ class DraftCase:
 
     def y_rows(self, s):
         no = self.new_offsets.tolist()
-        return bits(self.y_new[no[s]:no[s + 1]])
+        return bits(self.y_new[no[s]:no[s] + self.new[s]])
 
     def oracle_inputs(self):
         ys = [self.y_rows(s) for s in range(len(self.ctx))]

@@ -151,6 +151,31 @@ def test_cold_rows_projected_into_the_cache_by_the_gemm_epilogue():
     torch.cuda.empty_cache()
 
 
+def test_device_row_counts_through_the_gemm_epilogue():
+    """Device row counts on 8192 rows (4096 per sequence, 3000 and 1 of them new): the
+    cold rows go through the projection GEMM's K/V epilogue, the rows past each count are
+    neither stored nor used (the oracle sees only the new rows), and every cache row past
+    a sequence's context keeps what it held."""
+    wl = synth.small_bf16()
+    case = DraftCase(wl, [3050, 701], [3000, 1], sub=16, paged=True, spare_pages=2, stride=4096)
+    dr = wl.drafter
+
+    def tails():
+        out = []
+        for s, T in enumerate(case.ctx):
+            n_rows = len(case.pages[s]) * 64
+            for l in range(dr.n_layers):
+                kk, vv = hdf.read_kv_rows_paged(case.kv_k, case.kv_vt, l, case.pages[s], n_rows)
+                out.append((bits(kk[T:].contiguous()), bits(vv[T:].contiguous())))
+        return out
+    before = tails()
+    _compare(case, seqs=[0, 1])
+    for (kb, vb), (ka, va) in zip(before, tails()):
+        assert np.array_equal(kb, ka) and np.array_equal(vb, va)
+    del case
+    torch.cuda.empty_cache()
+
+
 def test_paged_cache_scattered_pages():
     """Paged cache: every sequence's 64-row tiles sit at random pages of a shared pool
     (with spare pages in between); warm and cold rows, ragged lengths, one and two
