@@ -123,7 +123,9 @@ attn_bf16_kernel(AttnArgs a, bf16_t* __restrict__ out) {
   // K operands of the four 16-key sub-tiles: sub-tile st = 2*ks + p, row r -> key
   // 32ks + 8(r/4) + 4p + r%4 of the tile (the order of the cache tile layout); each
   // operand is 64 lanes x 16 contiguous bytes.  V^T operands: lane holds
-  // V^T[16dt + ql][32ks + 8g .. +7].
+  // V^T[16dt + ql][32ks + 8g .. +7].  Each key and value is read once a call: the loads are
+  // non-temporal (measured: 8 x 2048 positions 54 -> 49 us, the ragged step's 1533 ->
+  // 1438 us).
   bf16x8_t kf[4][NJ];
   u32x4 vf[2][NDT];
   auto load_k = [&](int i) {
@@ -132,14 +134,14 @@ attn_bf16_kernel(AttnArgs a, bf16_t* __restrict__ out) {
     for (int st = 0; st < 4; ++st)
 #pragma unroll
       for (int j = 0; j < NJ; ++j)
-        kf[st][j] = __builtin_bit_cast(bf16x8_t, ld16(kt + (st * NJ + j) * 512));
+        kf[st][j] = __builtin_bit_cast(bf16x8_t, ld_nt16(kt + (st * NJ + j) * 512));
   };
   auto load_v = [&](int i) {
     const bf16_t* vt = v_src(i);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) vf[ks][dt] = ld16(vt + (ks * NDT + dt) * 512);
+      for (int dt = 0; dt < NDT; ++dt) vf[ks][dt] = ld_nt16(vt + (ks * NDT + dt) * 512);
   };
   for (int i = wid; i < ntiles; i += kAttnWaves) {
     load_k(i);
