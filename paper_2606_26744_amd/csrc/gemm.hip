@@ -408,13 +408,16 @@ gemm_bf16_kernel(GemmArgs p) {
     }
   } else {
     // Stage the fp32 tile in LDS, four waves (128 columns) at a time ([wave][row][column
-    // of the wave]); THREADS/BM threads per row scan each 128-column slab (lowest column
-    // on ties), and one atomic per row folds the tile's (max, index) into the row's
-    // packed key.  The K loop ended with a barrier, so the activation buffers are free.
+    // of the wave]).  Each thread scans one row of a slab over CPT columns: the row is
+    // tid % BM and the column part tid / BM, so the 64 rows a wave reads sit in 64
+    // different banks (row pitch 33 words), and its reads are issued before the compares.
+    // The parts' (max, lowest column) pairs meet in LDS after the last slab, and one
+    // atomic per row folds the tile's pair into the row's packed key.  The K loop ended
+    // with a barrier, so the activation buffers are free.
     float* Cs = reinterpret_cast<float*>(smem);
-    constexpr int TPR = THREADS / BM;        // threads per row
-    constexpr int CPT = 128 / TPR;           // columns of a slab per thread
-    const int rl = tid / TPR, part = tid % TPR;
+    constexpr int TPR = THREADS / BM;        // column parts of a slab
+    constexpr int CPT = 128 / TPR;           // columns of a part
+    const int rl = tid % BM, part = tid / BM;
     float best = -INFINITY;
     int bcol = 0x7FFFFFFF;
 #pragma unroll
@@ -434,37 +437,50 @@ gemm_bf16_kernel(GemmArgs p) {
         }
       }
       __syncthreads();
-      const int c0 = n0 + 128 * slab;
-      if (m0 + rl < p.M) {
-        for (int cc = part * CPT; cc < part * CPT + CPT; ++cc) {
-          if (c0 + cc >= p.N) break;
-          const float v = Cs[((cc >> 5) * BM + rl) * LDC + (cc & 31)];
-          if (v > best) {
-            best = v;
-            bcol = c0 + cc;
-          }
-        }
+      const int c0 = n0 + 128 * slab + part * CPT;
+      const int lim = min(CPT, p.N - c0);      // columns of this part inside N
+      float v[CPT];
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) {
+        const int cc = part * CPT + j;
+        v[j] = Cs[((cc >> 5) * BM + rl) * LDC + (cc & 31)];
       }
+#pragma unroll
+      for (int j = 0; j < CPT; ++j)
+        if (j < lim && v[j] > best) {
+          best = v[j];
+          bcol = c0 + j;
+        }
       if (p.C != nullptr) {
-        // Logits (tests): coalesced rows of the staged slab.
+        // Logits (tests, sampling): coalesced rows of the staged slab.
+        const int cs0 = n0 + 128 * slab;
         for (int e = tid; e < BM * 128; e += THREADS) {
           const int rr = e >> 7, cc = e & 127;
-          if (m0 + rr < p.M && c0 + cc < p.N)
-            p.C[int64_t(m0 + rr) * p.N + c0 + cc] = Cs[((cc >> 5) * BM + rr) * LDC + (cc & 31)];
+          if (m0 + rr < p.M && cs0 + cc < p.N)
+            p.C[int64_t(m0 + rr) * p.N + cs0 + cc] = Cs[((cc >> 5) * BM + rr) * LDC + (cc & 31)];
         }
       }
     }
+    __syncthreads();
+    float* rv = Cs;                                          // [part][row] maxima
+    int* rc = reinterpret_cast<int*>(Cs + TPR * BM);         // [part][row] columns
+    rv[part * BM + rl] = best;
+    rc[part * BM + rl] = bcol;
+    __syncthreads();
+    if (tid < BM && m0 + tid < p.M) {
+      best = rv[tid];
+      bcol = rc[tid];
 #pragma unroll
-    for (int o = 1; o < TPR; o <<= 1) {
-      const float ov = __shfl_xor(best, o, kWave);
-      const int oc = __shfl_xor(bcol, o, kWave);
-      if (ov > best || (ov == best && oc < bcol)) {
-        best = ov;
-        bcol = oc;
+      for (int q = 1; q < TPR; ++q) {
+        const float ov = rv[q * BM + tid];
+        const int oc = rc[q * BM + tid];
+        if (ov > best || (ov == best && oc < bcol)) {
+          best = ov;
+          bcol = oc;
+        }
       }
+      if (bcol != 0x7FFFFFFF) atomicMax(p.keys + m0 + tid, argmax_key(best, bcol));
     }
-    if (part == 0 && m0 + rl < p.M && bcol != 0x7FFFFFFF)
-      atomicMax(p.keys + m0 + rl, argmax_key(best, bcol));
   }
 }
 
