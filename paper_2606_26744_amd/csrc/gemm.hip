@@ -20,9 +20,10 @@
 //
 // Epilogues:
 //   PARTIAL  fp32 C (or split-K partial z at C + z*M*N) straight from registers
-//   ARGMAX   LM head: per row (max, lowest index) reduced across lanes, then across
-//            the four waves in LDS, folded into a packed 64-bit key with one atomicMax
-//            per row and tile; the logits are stored only when asked for
+//   ARGMAX   LM head: the transposed product, so that per row (max, lowest index) is
+//            taken over a lane's registers, then across the two lane halves and the
+//            waves in LDS, and folded into a packed 64-bit key with one atomicMax per
+//            row and tile; the logits are stored only when asked for
 //
 // fp32 (small correctness-size workloads): a plain LDS-tiled VALU kernel reading the
 // same packed weight layout, with the same epilogues.
@@ -127,6 +128,15 @@ gemm_bf16_kernel(GemmArgs p) {
              (int64_t(grp) * (p.K >> 4) * 4 + (blk & 3)) * 512 + lane * 8;
   }
 
+  // Argmax tiles compute the transposed product (the weights as the A operand): a lane
+  // then holds 16 columns of one row per 32-column block, and the row maxima are taken
+  // in registers.  Every other tile holds C = A.W^T (a lane: one column, 16 rows).
+  auto mma = [](bf16x8_t act, bf16x8_t w, f32x16_t c) {
+    if constexpr (EPI == kEpiArgmax)
+      return __builtin_amdgcn_mfma_f32_32x32x16_bf16(w, act, c, 0, 0, 0);
+    else
+      return __builtin_amdgcn_mfma_f32_32x32x16_bf16(act, w, c, 0, 0, 0);
+  };
   f32x16_t acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
@@ -203,9 +213,8 @@ gemm_bf16_kernel(GemmArgs p) {
           for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int tn = 0; tn < TN; ++tn)
-              acc[i][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                  af[ss][i], __builtin_bit_cast(bf16x8_t, rb[slot][ss * TN + tn]), acc[i][tn],
-                  0, 0, 0);
+              acc[i][tn] = mma(af[ss][i], __builtin_bit_cast(bf16x8_t, rb[slot][ss * TN + tn]),
+                               acc[i][tn]);
         __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
       };
@@ -262,8 +271,7 @@ gemm_bf16_kernel(GemmArgs p) {
               *reinterpret_cast<const bf16x8_t*>(&As[buf][arow + 32 * i][q * 16 + kof]);
 #pragma unroll
           for (int tn = 0; tn < TN; ++tn)
-            acc[i][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                af, __builtin_bit_cast(bf16x8_t, bq[q * TN + tn]), acc[i][tn], 0, 0, 0);
+            acc[i][tn] = mma(af, __builtin_bit_cast(bf16x8_t, bq[q * TN + tn]), acc[i][tn]);
         }
       }
     };
@@ -407,52 +415,63 @@ gemm_bf16_kernel(GemmArgs p) {
       }
     }
   } else {
-    // Stage the fp32 tile in LDS, four waves (128 columns) at a time ([wave][row][column
-    // of the wave]).  Each thread scans one row of a slab over CPT columns: the row is
-    // tid % BM and the column part tid / BM, so the 64 rows a wave reads sit in 64
-    // different banks (row pitch 33 words), and its reads are issued before the compares.
-    // The parts' (max, lowest column) pairs meet in LDS after the last slab, and one
-    // atomic per row folds the tile's pair into the row's packed key.  The K loop ended
-    // with a barrier, so the activation buffers are free.
+    // Transposed tile: lane l holds row 32i + l%32 and, of 32-column block b, columns
+    // 32b + 8(r/4) + 4(l/32) + r%4 (r = 0..15).  Each lane scans its columns in increasing
+    // order (lowest column on ties), the two lane halves of a row meet by a shuffle, the
+    // waves' (max, column) pairs meet in LDS, and one atomic per row folds the tile's pair
+    // into the row's packed key.  The K loop ended with a barrier, so LDS is free.
     float* Cs = reinterpret_cast<float*>(smem);
-    constexpr int TPR = THREADS / BM;        // column parts of a slab
-    constexpr int CPT = 128 / TPR;           // columns of a part
-    const int rl = tid % BM, part = tid / BM;
-    float best = -INFINITY;
-    int bcol = 0x7FFFFFFF;
+    const int tok = lane & 31;
+    float best[TM];
+    int bcol[TM];
 #pragma unroll
-    for (int slab = 0; slab < NB / 4; ++slab) {
-      if (slab > 0) __syncthreads();
+    for (int i = 0; i < TM; ++i) {
+      best[i] = -INFINITY;
+      bcol[i] = 0x7FFFFFFF;
+    }
 #pragma unroll
-      for (int tn = 0; tn < TN; ++tn) {
-        const int b = wid * TN + tn;            // this wave's block inside the tile
-        if ((b >> 2) == slab) {
+    for (int tn = 0; tn < TN; ++tn) {
+      const int cb = n0 + 32 * (wid * TN + tn) + 4 * (lane >> 5);
 #pragma unroll
-          for (int i = 0; i < TM; ++i)
+      for (int r = 0; r < 16; ++r) {
+        const int col = cb + 8 * (r >> 2) + (r & 3);
+        const bool in = col < p.N;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int rr = 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-              Cs[((b & 3) * BM + rr) * LDC + (lane & 31)] = acc[i][tn][r];
-            }
-        }
+        for (int i = 0; i < TM; ++i)
+          if (in && acc[i][tn][r] > best[i]) {
+            best[i] = acc[i][tn][r];
+            bcol[i] = col;
+          }
       }
-      __syncthreads();
-      const int c0 = n0 + 128 * slab + part * CPT;
-      const int lim = min(CPT, p.N - c0);      // columns of this part inside N
-      float v[CPT];
+    }
 #pragma unroll
-      for (int j = 0; j < CPT; ++j) {
-        const int cc = part * CPT + j;
-        v[j] = Cs[((cc >> 5) * BM + rl) * LDC + (cc & 31)];
+    for (int i = 0; i < TM; ++i) {
+      const float ov = __shfl_xor(best[i], 32, kWave);
+      const int oc = __shfl_xor(bcol[i], 32, kWave);
+      if (ov > best[i] || (ov == best[i] && oc < bcol[i])) {
+        best[i] = ov;
+        bcol[i] = oc;
       }
+    }
+    if (p.C != nullptr) {
+      // Logits (tests, sampling): the tile goes through LDS four waves (128 columns) at a
+      // time ([block][row][column of the block]) and leaves as coalesced rows.
 #pragma unroll
-      for (int j = 0; j < CPT; ++j)
-        if (j < lim && v[j] > best) {
-          best = v[j];
-          bcol = c0 + j;
+      for (int slab = 0; slab < NB / 4; ++slab) {
+        if (slab > 0) __syncthreads();
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) {
+          const int b = wid * TN + tn;
+          if ((b >> 2) == slab) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+              for (int r = 0; r < 16; ++r)
+                Cs[((b & 3) * BM + 32 * i + tok) * LDC + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)] =
+                    acc[i][tn][r];
+          }
         }
-      if (p.C != nullptr) {
-        // Logits (tests, sampling): coalesced rows of the staged slab.
+        __syncthreads();
         const int cs0 = n0 + 128 * slab;
         for (int e = tid; e < BM * 128; e += THREADS) {
           const int rr = e >> 7, cc = e & 127;
@@ -460,26 +479,31 @@ gemm_bf16_kernel(GemmArgs p) {
             p.C[int64_t(m0 + rr) * p.N + cs0 + cc] = Cs[((cc >> 5) * BM + rr) * LDC + (cc & 31)];
         }
       }
+      __syncthreads();
+    }
+    float* rv = Cs;                                          // [wave][row] maxima
+    int* rc = reinterpret_cast<int*>(Cs + NW * BM);          // [wave][row] columns
+    if (lane < 32) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        rv[wid * BM + 32 * i + tok] = best[i];
+        rc[wid * BM + 32 * i + tok] = bcol[i];
+      }
     }
     __syncthreads();
-    float* rv = Cs;                                          // [part][row] maxima
-    int* rc = reinterpret_cast<int*>(Cs + TPR * BM);         // [part][row] columns
-    rv[part * BM + rl] = best;
-    rc[part * BM + rl] = bcol;
-    __syncthreads();
     if (tid < BM && m0 + tid < p.M) {
-      best = rv[tid];
-      bcol = rc[tid];
+      float bv = rv[tid];
+      int bc = rc[tid];
 #pragma unroll
-      for (int q = 1; q < TPR; ++q) {
-        const float ov = rv[q * BM + tid];
-        const int oc = rc[q * BM + tid];
-        if (ov > best || (ov == best && oc < bcol)) {
-          best = ov;
-          bcol = oc;
+      for (int w = 1; w < NW; ++w) {
+        const float ov = rv[w * BM + tid];
+        const int oc = rc[w * BM + tid];
+        if (ov > bv || (ov == bv && oc < bc)) {
+          bv = ov;
+          bc = oc;
         }
       }
-      if (bcol != 0x7FFFFFFF) atomicMax(p.keys + m0 + tid, argmax_key(best, bcol));
+      if (bc != 0x7FFFFFFF) atomicMax(p.keys + m0 + tid, argmax_key(bv, bc));
     }
   }
 }
