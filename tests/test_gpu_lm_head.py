@@ -83,6 +83,31 @@ def test_ties_take_lowest_index():
     assert lg[0, 17].item() == lg[0, 1200].item() == lg[0, 2999].item()
 
 
+@pytest.mark.parametrize("M", [4, 100, 136])
+def test_ties_inside_one_tile_take_lowest_index(M):
+    """Tied columns inside one 512-column tile, one pair per row, placed so that each
+    level of the tile's (max, lowest index) combine decides one pair: the same lane
+    (33 vs 40), the two lane halves (4 vs 8), the two 32-column blocks of a wave (20 vs
+    36) and different waves (70 vs 200).  M = 4 runs 64-row tiles, M = 100 one 128-row
+    tile, M = 136 two row tiles (the tie rows repeat in the second one)."""
+    d, V = 128, 3000
+    pairs = [(4, 8), (33, 40), (20, 36), (70, 200)]      # (expected, tied higher column)
+    hid, w = _inputs(M, d, V, "bf16", 65)
+    for lo, hi in pairs:
+        w[hi] = w[lo]
+    rows = list(range(len(pairs))) + ([130 + i for i in range(len(pairs))] if M > 128 else [])
+    for r in rows:
+        lo = pairs[r % 130][0]
+        hid[r] = (w[lo].float() * 40).to(torch.bfloat16)
+    print(f"[lm_head ties] M={M}", flush=True)
+    am, _, lg = hdf.lm_head_argmax(hid, hdf.pack_weight(w), want_logits=True)
+    torch.cuda.synchronize()
+    for r in rows:
+        lo, hi = pairs[r % 130]
+        assert lg[r, lo].item() == lg[r, hi].item() == lg[r].max().item(), (r, lo, hi)
+        assert am[r].item() == lo, (r, am[r].item(), lo)
+
+
 def test_pack_weight_layout():
     """The packed layout puts (n, k) at (((n/128)(K/16) + k/16)*4 + (n%128)/32)*512
     + ((n%32) + 32((k%16)/8))*8 + k%8 and pads rows to a multiple of 128 with zeros."""
