@@ -29,7 +29,7 @@ HBM_PEAK_GBS = 8000.0
 # profiles/lm_head_argmax_hbm_counters.md (FETCH_SIZE x 2.049 + WRITE_SIZE x 1.025, the
 # factors a plain device copy of known size gives).  Valid only for the kernel source it
 # was measured on: reported as null once gemm.hip or common.hpp changes.
-LM_HEAD_TRAFFIC = {"source_sha": "b9a2048469cfd0ec", "bytes": (532826.1 * 2.049 + 253.0 * 1.025) * 1024}
+LM_HEAD_TRAFFIC = {"source_sha": "468c2a931409e247", "bytes": (532898.7 * 2.049 + 253.0 * 1.025) * 1024}
 BF16_PEAK_TFLOPS = 2500.0
 METRIC = "draft blocks/sec at d=4096,B=16,V=129280; reducer HBM GB/s; MFMA util %"
 

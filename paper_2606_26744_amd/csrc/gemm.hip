@@ -674,7 +674,7 @@ static hipError_t launch_gemm_any(bool bf16, int epi, const GemmArgs& a, GemmPla
       } else if (plan.nw == 8) {
         launch_bf16_partial<8, 1>(a, plan.splits, s);
       } else if (plan.nw == 6) {
-        launch_bf16_partial<6, 1>(a, plan.splits, s);
+        launch_bf16_partial<6, 1, 3>(a, plan.splits, s);
       } else {
         launch_bf16_partial<4, 1, 2>(a, plan.splits, s);
       }
