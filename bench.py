@@ -29,7 +29,7 @@ HBM_PEAK_GBS = 8000.0
 # profiles/lm_head_argmax_hbm_counters.md (FETCH_SIZE x 2.049 + WRITE_SIZE x 1.025, the
 # factors a plain device copy of known size gives).  Valid only for the kernel source it
 # was measured on: reported as null once gemm.hip or common.hpp changes.
-LM_HEAD_TRAFFIC = {"source_sha": "468c2a931409e247", "bytes": (532898.7 * 2.049 + 253.0 * 1.025) * 1024}
+LM_HEAD_TRAFFIC = {"source_sha": "551d54ecdc622c82", "bytes": (532898.7 * 2.049 + 253.0 * 1.025) * 1024}
 BF16_PEAK_TFLOPS = 2500.0
 METRIC = "draft blocks/sec at d=4096,B=16,V=129280; reducer HBM GB/s; MFMA util %"
 
@@ -406,10 +406,21 @@ def blas_reference(torch):
 
 
 def _kernel_source_sha():
+    """Hash of the LM-head kernel's code (gemm.hip + common.hpp) with comments and
+    blank space removed, so that the measured traffic stays attached to the code it was
+    measured on and not to its comments."""
     import hashlib
+    import re
+
+    def code(path):
+        text = open(path).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        return "\n".join(l.strip() for l in text.splitlines() if l.strip())
+
     c = os.path.join(ROOT, "paper_2606_26744_amd", "csrc")
-    data = open(os.path.join(c, "gemm.hip"), "rb").read() + open(os.path.join(c, "common.hpp"), "rb").read()
-    return hashlib.sha256(data).hexdigest()[:16]
+    data = code(os.path.join(c, "gemm.hip")) + "\n" + code(os.path.join(c, "common.hpp"))
+    return hashlib.sha256(data.encode()).hexdigest()[:16]
 
 
 def cpu_baseline(torch, synth, wl, h, w, red, args, offs):

@@ -10,11 +10,12 @@
 // with one contiguous 1 KB load per instruction, the four waves of a workgroup read
 // one contiguous 16 KB run per 64-k step, and no weight byte passes through LDS.
 //
-// bf16 weight-streaming kernel: 4 waves, each owning 32 output columns and all BM
-// rows (BM = 128, or 64 when M <= 64) of a 128-column tile.  The activation slice
-// (BM x 64) is shared through a double-buffered, padded LDS tile.  A ring of
-// STAGES K-steps of weights is in flight per wave; activations are fetched one step
-// further ahead than weights because memory counters complete in issue order.
+// bf16 kernel: NW waves (4, 6 or 8), each owning TN 32-column blocks (1, or 2 for the
+// matrix-core bound shapes and the LM head) and all BM rows (BM = 128, or 64 when
+// M <= 64) of a 32*NW*TN-column tile.  The activation slice (BM x 64) is shared
+// through a double-buffered, padded LDS tile.  A ring of STAGES K-steps of weights is
+// in flight per wave; activations are fetched one step further ahead than weights
+// because memory counters complete in issue order.
 // Split-K runs over gridDim.z; tiles are ordered so that the M-tiles of one weight
 // column block run on the same XCD back to back (its L2 serves the re-reads).
 //
@@ -77,8 +78,9 @@ gemm_bf16_kernel(GemmArgs p) {
   constexpr int A_CH = (A_CHUNKS + THREADS - 1) / THREADS;
   constexpr int LDC = 33;                         // padded row of a wave's 32 columns
   static_assert(EPI == kEpiPartial || NB % 4 == 0, "argmax and K/V tiles are whole 128-column slabs");
-  // LDS: the double-buffered activation tile, reused after the K loop by the ARGMAX
-  // epilogue to stage the fp32 tile of four waves at a time ([wave][row][32 columns]).
+  // LDS: the activation buffers, reused after the K loop by the K/V epilogue and the
+  // ARGMAX epilogue's logits to stage the fp32 tile 128 columns at a time ([block][row]
+  // [32 columns]), and by the ARGMAX epilogue's per-wave row maxima.
   constexpr size_t kMainLds = PP ? size_t(4) * BM * (32 + 8) * sizeof(bf16_t)   // NBUF units
                                 : size_t(2) * BM * LDA * sizeof(bf16_t);
   constexpr size_t kEpiLds = (EPI != kEpiPartial) ? size_t(4) * BM * LDC * sizeof(float) : 0;
