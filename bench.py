@@ -37,8 +37,8 @@ METRIC = "draft blocks/sec at d=4096,B=16,V=129280; reducer HBM GB/s; MFMA util 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-reducer-stress", action="store_true")
     ap.add_argument("--no-m-sweep", action="store_true")
