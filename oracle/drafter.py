@@ -6,8 +6,8 @@ The paper fixes what the drafter consumes and predicts, not its layers:
     Sec. 2.1);
   * the context is the target's pre-collapse residual reduced by the gated
     reducer and injected into the drafter (Sec. 2.1, Sec. 2.2, Fig. 2 caption);
-  * for a block anchored at position a, draft position k predicts the token at
-    a+k (Sec. 2.3).
+  * slot k of a block whose anchor sits at index a targets token index a+k
+    (Sec. 2.3).
 
 Readings taken for the layer itself (listed in the design notes): pre-norm
 transformer layers with multi-head attention (n_heads * head_dim = d) and a

@@ -1,9 +1,9 @@
 """Oracle of the LM-head KL distillation forward (Sec. 2.4).  Test infrastructure
 only.
 
-For a block anchored at position a, draft position k (predicting the token at a+k)
-is supervised by the teacher distribution LMHead(h_{a+k-1}); only the first P block
-positions are distilled:
+Index convention (Sec. 2.3): with a the anchor's position, slot k of the block targets
+token index a+k, and its teacher is LMHead applied to the target's state at index
+a+k-1.  Only slots k = 1..P enter the loss:
     L_KL = T^2 / P * sum_{k=1..P} E_blocks[ KL(p_k^T || q_k^T) ]
     L    = L_CE + alpha * L_KL
 with p^T, q^T the softmax of teacher and draft logits divided by T (Hinton's T^2

@@ -57,6 +57,19 @@ class PagePool:
         return len(self._free)
 
 
+def pages_for(lengths, max_ctx: int) -> np.ndarray:
+    """Pages of 64 rows that context lengths `lengths` occupy.  Raises ValueError when a
+    length exceeds max_ctx: the drafter call is made with max_ctx, which also bounds the
+    RoPE table (max_ctx + B rows), so a longer context would read past that table even
+    where its last page still has room."""
+    lengths = np.asarray(lengths, dtype=np.int64)
+    over = np.nonzero(lengths > max_ctx)[0]
+    if over.size:
+        s = int(over[0])
+        raise ValueError(f"sequence {s} outgrows max_ctx={max_ctx} (length {int(lengths[s])})")
+    return (lengths + 63) // 64
+
+
 class PagedDecoder:
     """Decoding state of n_seq sequences: a paged KV cache, each sequence's pages and
     context length, the block tokens (anchor + masks) and the step buffers."""
@@ -123,10 +136,9 @@ class PagedDecoder:
 
     def _grow(self, new_counts: np.ndarray):
         self._copied.synchronize()          # the staging buffer is free again
+        need_all = pages_for(self.ctx + new_counts, self.max_ctx)
         for s in range(self.n_seq):
-            need = (int(self.ctx[s]) + int(new_counts[s]) + 63) // 64
-            if need > self.max_pages:
-                raise ValueError(f"sequence {s} outgrows max_ctx={self.max_ctx}")
+            need = int(need_all[s])
             while len(self.pages[s]) < need:
                 p = self.pool.take()
                 self._pt_host[s, len(self.pages[s])] = p
@@ -202,12 +214,9 @@ class PagedDecoder:
     def _reserve(self):
         """Pages for every position below the upper bound; the page table goes to the
         device through a staging buffer no pending copy still reads."""
-        need = (self._ctx_hi + 63) // 64
-        if (need > self.max_pages).any():
+        if (self._ctx_hi > self.max_ctx).any():
             self._tighten(wait=True)
-            need = (self._ctx_hi + 63) // 64
-            if (need > self.max_pages).any():
-                raise ValueError(f"a sequence outgrows max_ctx={self.max_ctx}")
+        need = pages_for(self._ctx_hi, self.max_ctx)
         changed = False
         for s in range(self.n_seq):
             while len(self.pages[s]) < need[s]:
