@@ -11,14 +11,18 @@ exceeds 2e-2 (|ref| >= 4).
 import numpy as np
 
 # End-to-end bounds for the drafter's bf16 chain, set from the measured spread of the
-# oracle under 1e-7 relative perturbations of its pre-rounding values
-# (tests/test_bf16_chain_sensitivity.py: row RMS ~5e-3, logits ~1.5e-2 at the small
-# configuration): twice the spread.
+# oracle itself when every pre-rounding value is perturbed by a relative 1e-7 (small
+# configuration) or 1e-6 (the full-size shape, d=4096, V=129280; the size of an fp32
+# dot product's rounding error over K = 4096), tests/test_bf16_chain_sensitivity.py.
+# Measured at full size: block-state row RMS up to 4e-3 (6e-3 at 4e-6), logits up to
+# 2.5e-2 (3.4e-2 at 4e-6), argmax flips only on rows whose top-2 margin is below 3.2e-3.
 STATE_RMS_REL = 1e-2      # block states / cached K,V: per-row RMS difference / RMS
 STATE_ABS = 4e-2          # ... and elementwise max(STATE_ABS, STATE_ULPS ulp)
 STATE_ULPS = 4
 E2E_LOGIT_ABS = 5e-2      # logits of a whole step (the LM head alone meets 2e-2)
-E2E_MARGIN = 5e-2         # argmax compared where the oracle's top-2 margin clears this
+E2E_MARGIN = 2e-2         # end-to-end argmax compared where the oracle's top-2 margin
+                          # clears this; below it the GPU's pick must be a near-tie
+STAGE_MARGIN = 1e-2       # the LM-head stage on identical inputs (the stated bound)
 
 
 def bf16_ulp(x):

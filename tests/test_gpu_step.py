@@ -1,13 +1,25 @@
 """End-to-end parity of one drafter step (reduce -> draft block -> LM head argmax ->
-accept) on the GPU against the oracle chain on the CPU.
+accept) on the GPU against the oracle chain on the CPU, over every sequence of the
+batch.
 
-The LM head alone meets 2e-2 on logits and exact argmax outside 1e-2 margins
-(test_gpu_lm_head).  Across a whole step the bf16 storage chain spreads correct results
-further apart (tests/test_bf16_chain_sensitivity.py), so here logits are held to
-E2E_LOGIT_ABS and argmax tokens are compared bit-exactly where the oracle's top-2 margin
-clears E2E_MARGIN; an acceptance length is compared only when every draft position it
-depends on clears that margin.  fp32 workloads keep the 1e-4 relative bounds and 1e-2
-margins."""
+Three comparisons per step:
+  1. Stage parity of the LM head on identical inputs: the oracle's LM head applied to
+     the GPU's own block states.  Logits within 2e-2 (bf16) / 1e-4 relative (fp32) and
+     argmax bit-exact wherever that oracle's top-2 margin is >= 1e-2 (the stated bound),
+     on at least 80% of the rows.
+  2. The whole chain against the oracle run from scratch on the same inputs.  Reduced
+     rows at the reducer's bounds, block states at the bf16-chain bounds, logits within
+     E2E_LOGIT_ABS, argmax bit-exact wherever the oracle's margin is >= E2E_MARGIN (at
+     least 80% of the rows).  On every other row the GPU's pick must be a near-tie: its
+     oracle logit within E2E_MARGIN of the oracle's maximum.
+  3. Acceptance: the GPU's accept_len, next_anchor and commits equal oracle.accept on
+     the GPU's own drafts for every sequence (integer stage, bit-exact), and equal the
+     from-scratch oracle's for every sequence.  The synthetic targets copy the oracle's
+     drafts with the workload's probability; at a slot whose oracle margin is below
+     E2E_MARGIN the target is the oracle's lowest-logit token instead, outside the
+     slot's near-tie set, so both sides reject there whatever near-tie they pick and
+     every acceptance length is comparable (the same holds for uniform targets).
+The bounds and their derivation are in tests/_tol.py."""
 import numpy as np
 import pytest
 import torch
@@ -21,39 +33,44 @@ from oracle.numerics import as_f64
 from paper_2606_26744_amd import hdf
 from paper_2606_26744_amd.step import StepBuffers, drafter_step
 from tests._case import DraftCase, bits
-from tests._tol import (E2E_LOGIT_ABS, E2E_MARGIN, assert_abs_close, assert_bf16_close,
-                        assert_bf16_state_close, assert_f32_rows_close)
+from tests._tol import (E2E_LOGIT_ABS, E2E_MARGIN, STAGE_MARGIN, assert_abs_close,
+                        assert_bf16_close, assert_bf16_state_close, assert_f32_rows_close)
 
 pytestmark = pytest.mark.gpu
 
 
-def _step_case(wl, ctx, new, *, seqs, sub=0, uniform_targets=False):
-    print(f"[step] {wl.name} ctx={ctx[:6]} new={new[:6]} seqs={seqs}", flush=True)
+def _step_case(wl, ctx, new, *, sub=0, uniform_targets=False):
+    n_seq = len(ctx)
+    seqs = list(range(n_seq))
+    print(f"[step] {wl.name} n_seq={n_seq} ctx={ctx[:8]} new={new[:8]}", flush=True)
     n_new = sum(new)
     red = synth.reducer_inputs(wl, n_new, device="cuda", sub=sub)
     case = DraftCase(wl, ctx, new, random_norms=False, sub=sub,
                      y_from=torch.empty((n_new, wl.d), dtype=red["H"].dtype, device="cuda"))
     B = case.B
-    n_seq = len(ctx)
+    bf = wl.dtype == "bf16"
     W = case.oracle_weights()
+    wlm = bits(case.w["w_lm"])
     no = case.new_offsets.tolist()
     Hn = bits(red["H"])
     Wg, bg = bits(red["W_g"]), bits(red["b_g"])
-    # Oracle chain for the sampled sequences: reduce -> draft block -> LM head.
-    ys = {s: ref_reduce(Hn[no[s]:no[s + 1]], Wg, bg, dtype=wl.dtype)[0] for s in seqs}
+    # Oracle chain from scratch: reduce -> draft block -> LM head.
+    ys = [ref_reduce(Hn[no[s]:no[s + 1]], Wg, bg, dtype=wl.dtype)[0] for s in seqs]
     toks = bits(case.tokens)
-    hid_ref = ref_draft(W, [ys.get(s) for s in range(n_seq)], toks, kv_prefix=case.prefix,
-                        seqs=seqs)
-    am_ref, lg_ref, margin = ref_lm(hid_ref, bits(case.w["w_lm"]))
-    drafts_ref = am_ref.reshape(len(seqs), B)[:, 1:]
-    # Targets: sampled sequences copy the oracle's drafts with the workload's probability;
-    # the others get uniform tokens (they are not checked).
+    hid_ref = ref_draft(W, ys, toks, kv_prefix=case.prefix)
+    am_ref, lg_ref, margin = ref_lm(hid_ref, wlm)
+    drafts_ref = am_ref.reshape(n_seq, B)[:, 1:]
+    MARGIN = E2E_MARGIN if bf else STAGE_MARGIN
     V = wl.drafter.vocab
-    rng = np.random.default_rng([wl.seed, 99, sub])
-    targets = rng.integers(0, V, (n_seq, B)).astype(np.int32)
-    if not uniform_targets:
-        p = [(wl.match_p or [0.8] * n_seq)[s] for s in seqs]
-        targets[seqs] = synth.make_targets(drafts_ref, p, V, seed=wl.seed, sub=sub)
+    if uniform_targets:
+        rng = np.random.default_rng([wl.seed, 99, sub])
+        targets = rng.integers(0, V, (n_seq, B)).astype(np.int32)
+    else:
+        targets = synth.make_targets(drafts_ref, wl.match_p or [0.8] * n_seq, V, seed=wl.seed,
+                                     sub=sub)
+    near = margin.reshape(n_seq, B)[:, 1:] < MARGIN
+    low = np.argmin(lg_ref.reshape(n_seq, B, V)[:, 1:], axis=2).astype(np.int32)
+    targets[:, :B - 1] = np.where(near, low, targets[:, :B - 1])
     tg = torch.as_tensor(targets).cuda()
     bufs = StepBuffers(case.h, n_seq, B, n_new, case.max_ctx, wl.m)
     out = drafter_step(case.h, bufs, H_new=red["H"], W_g=red["W_g"], b_g=red["b_g"],
@@ -61,71 +78,93 @@ def _step_case(wl, ctx, new, *, seqs, sub=0, uniform_targets=False):
                        kv_offsets=case.kv_offsets, kv_k=case.kv_k, kv_vt=case.kv_vt,
                        tokens=case.tokens, targets=tg, logits=True)
     torch.cuda.synchronize()
+    M = n_seq * B
     # Reduced rows
     for s in seqs:
         y = bits(out["Y"][no[s]:no[s + 1]])
-        if wl.dtype == "bf16":
+        if bf:
             assert_bf16_close(as_f64(y), ys[s], "Y")
         else:
             assert_f32_rows_close(y, ys[s], "Y")
-    rows = np.concatenate([np.arange(s * B, (s + 1) * B) for s in seqs])
-    hid = bits(out["hidden"][torch.as_tensor(rows).cuda()])
-    lg = out["logits"][torch.as_tensor(rows).cuda()].cpu().numpy()
-    if wl.dtype == "bf16":
-        assert_bf16_state_close(as_f64(hid), hid_ref, "hidden")
+    hid = bits(out["hidden"])
+    lg = out["logits"][:M].cpu().numpy()
+    am = out["argmax"].cpu().numpy()[:M]
+    # 1. The LM-head stage on the GPU's own block states.
+    am_st, lg_st, mg_st = ref_lm(hid, wlm)
+    if bf:
+        assert_abs_close(lg, lg_st, 2e-2, "logits (LM-head stage)")
+    else:
+        assert_f32_rows_close(lg, lg_st, "logits (LM-head stage)")
+    ok_st = mg_st >= STAGE_MARGIN
+    assert np.array_equal(am[ok_st], am_st[ok_st]), np.nonzero(am[ok_st] != am_st[ok_st])
+    # 2. The whole chain against the oracle from scratch.
+    if bf:
+        _, worst = assert_bf16_state_close(as_f64(hid), hid_ref, "hidden")
         assert_abs_close(lg, lg_ref, E2E_LOGIT_ABS, "logits")
-        MARGIN = E2E_MARGIN
     else:
         assert_f32_rows_close(hid, hid_ref, "hidden")
         assert_f32_rows_close(lg, lg_ref, "logits")
-        MARGIN = 1e-2
-    am = out["argmax"].cpu().numpy()[rows]
+        worst = 0.0
     ok = margin >= MARGIN
-    assert np.array_equal(am[ok], am_ref[ok])
+    assert np.array_equal(am[ok], am_ref[ok]), np.nonzero(am[ok] != am_ref[ok])
+    # rows left out: the GPU's pick is one of the oracle's near-ties
+    z = lg_ref.astype(np.float64)
+    picked = z[np.arange(M), am]
+    near_ok = picked >= z.max(axis=1) - MARGIN
+    assert near_ok.all(), np.nonzero(~near_ok)
+    # 3. Acceptance: on the GPU's own drafts (always exact) and against the oracle chain.
     acc = out["accept_len"].cpu().numpy()
     anc = out["next_anchor"].cpu().numpy()
-    r_acc, r_anc, _, _ = ref_accept(drafts_ref, targets[seqs])
-    compared = 0
-    for i, s in enumerate(seqs):
-        mg = margin.reshape(len(seqs), B)[i, 1:]
-        j = min(acc[s], r_acc[i])
-        if np.all(mg[:min(j + 1, B - 1)] >= MARGIN):
-            assert acc[s] == r_acc[i] and anc[s] == r_anc[i], (s, acc[s], r_acc[i])
-            compared += 1
-    print(f"  argmax compared {int(ok.sum())}/{ok.size}, acceptance compared {compared}/{len(seqs)},"
-          f" accept lens {acc[seqs].tolist()}", flush=True)
-    # GPU commit bookkeeping is consistent with its own accept lengths
     offs = out["commit_offsets"].cpu().numpy()
-    assert np.array_equal(np.diff(offs), acc + 1)
+    ctoks = out["commit_tokens"].cpu().numpy()
+    g_acc, g_anc, g_offs, g_toks = ref_accept(am.reshape(n_seq, B)[:, 1:], targets)
+    assert np.array_equal(acc, g_acc) and np.array_equal(anc, g_anc)
+    assert np.array_equal(offs, g_offs) and np.array_equal(ctoks[:g_offs[-1]], g_toks)
+    r_acc, r_anc, _, _ = ref_accept(drafts_ref, targets)
+    assert np.array_equal(acc, r_acc) and np.array_equal(anc, r_anc), (acc, r_acc)
+    compared = n_seq
+    n_ok, n_st = int(ok.sum()), int(ok_st.sum())
+    dlog = float(np.abs(lg.astype(np.float64) - lg_ref).max())
+    print(f"  argmax: stage compared {n_st}/{M} (margin >= {STAGE_MARGIN}), end-to-end "
+          f"compared {n_ok}/{M} (margin >= {MARGIN}), near-ties validated {M - n_ok}; "
+          f"rows under 1e-2: {int((margin < 1e-2).sum())}, under 5e-2: "
+          f"{int((margin < 5e-2).sum())}; max |dlogit| end-to-end {dlog:.4f}, block-state "
+          f"row RMS {worst:.2e}; acceptance compared {compared}/{n_seq}, accept lens "
+          f"{acc.tolist()}", flush=True)
+    assert n_st >= 0.8 * M and n_ok >= 0.8 * M
+    assert compared >= 0.5 * n_seq
     return out
 
 
 def test_tiny_fp32_step():
     wl = synth.tiny_fp32()
-    _step_case(wl, [64], [64], seqs=[0], uniform_targets=True)
+    _step_case(wl, [64], [64], uniform_targets=True)
 
 
 def test_small_bf16_step_cold():
     wl = synth.small_bf16()
-    _step_case(wl, [512] * 4, [512] * 4, seqs=[0, 1, 2, 3])
+    _step_case(wl, [512] * 4, [512] * 4)
 
 
 def test_small_bf16_step_warm():
     wl = synth.small_bf16()
-    _step_case(wl, [512] * 4, [16] * 4, seqs=[0, 1, 2, 3], sub=1)
+    _step_case(wl, [512] * 4, [16] * 4, sub=1)
 
 
-def test_full_size_step_sampled():
-    """The benchmark's configuration: 8 x 2048 context, 16 new rows per sequence."""
+def test_full_size_step():
+    """The benchmark's configuration: 8 x 2048 context, 16 new rows per sequence, all
+    eight sequences."""
     wl = synth.drafter_full()
-    _step_case(wl, [2048] * 8, [16] * 8, seqs=[0, 7])
+    _step_case(wl, [2048] * 8, [16] * 8)
     torch.cuda.empty_cache()
 
 
-def test_ragged_step_subset():
+def test_ragged_step():
+    """Six sequences of the ragged workload (contexts from its U[1024, 16384] draw), every
+    one checked."""
     wl = synth.ragged_decode()
     ctx = wl.ctx_lens[:6]
-    _step_case(wl, ctx, [16] * 6, seqs=[int(np.argmin(ctx)), int(np.argmax(ctx))], sub=2)
+    _step_case(wl, ctx, [16] * 6, sub=2)
     torch.cuda.empty_cache()
 
 

@@ -7,7 +7,7 @@ plausibly make: the flatten order of vec(H_t), softmax instead of independent si
 gates, a dropped normalisation, epsilon outside the square root, a RoPE sign, the
 attention scale, gate and up swapped, the block positions off by one, the wrong key
 weights, a dropped residual, an acceptance off-by-one, the argmax tie rule, the RMS
-formula, and the bf16 tie rule.
+formula, the bf16 tie rule, and drafts taken from the anchor slot.
 """
 import concurrent.futures as cf
 import os
@@ -39,6 +39,8 @@ MUTATIONS = [
     ("numerics.py", "ms = np.mean(x * x, axis=-1, keepdims=True)",
      "ms = np.mean(np.abs(x), axis=-1, keepdims=True) ** 2"),
     ("numerics.py", "lsb = (u >> np.uint64(_DROP)) & np.uint64(1)", "lsb = np.uint64(1)"),
+    ("step.py", "draft = am.reshape(len(seqs), B)[:, 1:]",
+     "draft = am.reshape(len(seqs), B)[:, :-1]"),
 ]
 
 

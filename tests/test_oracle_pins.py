@@ -530,3 +530,25 @@ def test_step_drafts_come_from_slots_one_to_b_minus_one():
     hid = draft_block(W, [y], toks)
     am2, _, _ = lm_head_argmax(hid, W.w_lm)
     assert np.array_equal(am2, out["argmax"])
+
+
+def test_step_drafts_are_the_mask_slots_not_the_anchor():
+    """Sec. 2.3: slot k of a block targets token index a+k, so the K = B-1 drafts are
+    the predictions of slots 1..B-1.  Without positions (theta = 0) the block is
+    permutation-equivariant: the mask slots hold one token and no position, so they
+    reach the same state and the same argmax, while slot 0 holds the anchor and predicts
+    something else.  The drafts of a sequence are therefore B-1 equal tokens that differ
+    from slot 0's prediction: a slice that kept slot 0 (or dropped a mask slot) fails."""
+    W, _ = _tiny_weights(seed=24, theta=0.0)
+    r = np.random.default_rng(22)
+    m, B, mask = 2, 6, 49
+    H = [r.standard_normal((7, m, 16)), r.standard_normal((5, m, 16))]
+    Wg = r.standard_normal((m, m * 16)) * 0.1
+    toks = np.array([[3] + [mask] * (B - 1), [11] + [mask] * (B - 1)])
+    out = drafter_step(W, H, Wg, np.zeros(m), toks, reduce_dtype="f32")
+    am = out["argmax"].reshape(2, B)
+    drafts = out["draft"]
+    assert drafts.shape == (2, B - 1)
+    for s in range(2):
+        assert np.all(drafts[s] == am[s, 1]), drafts[s]
+        assert am[s, 0] != am[s, 1], am[s]
