@@ -205,6 +205,31 @@ hdf_status hdf_rope_table(float* out_host, int n_pos, int head_dim, double theta
  * >= kv_offsets[n_seq].  Rows past T_s inside a slot are never used. */
 size_t hdf_kv_cache_bytes(const hdf_drafter* w, int64_t kv_cap); /* bytes of k (= of vt) */
 
+/* Row-major keys and values to and from the cache layout above, one layer at a time:
+ * row i of k_rows / v_rows ([n_rows][n_heads*head_dim], keys after RoPE, head h in
+ * columns h*head_dim ..) is cache row rows[i] (device int32 [n_rows]), or row0 + i when
+ * rows is NULL.  With a paged cache (hdf_draft_block_paged) position p of a sequence is
+ * row page_table[s][p/64]*64 + p%64.  These let a caller that holds keys and values in
+ * row-major form (its own prefill, a cache saved elsewhere) fill or inspect a cache
+ * without reproducing the tile layout, which is this library's own (the attention
+ * kernel's operand order, not a layout the paper prescribes).
+ * kv_k, kv_vt  the whole cache [n_layers][n_heads][kv_cap/64][64*head_dim]; `layer`
+ *              selects the layer (0 <= layer < n_layers, not checked against the cache)
+ * Either pair (kv_k with k_rows, kv_vt with v_rows) may be NULL to skip keys or values,
+ * not both.  Writes touch only the cache rows named; reads of a row outside [0, kv_cap)
+ * (from `rows`) return zeros and writes to one are skipped.
+ * Limits: head_dim in {64, 128}; kv_cap a positive multiple of 64 below 2^31;
+ *         0 <= n_rows < 2^31 (0 is a no-op); without `rows`, row0 + n_rows <= kv_cap;
+ *         the tensors 16-byte aligned.  Rows named twice in one write: either wins. */
+hdf_status hdf_kv_write_rows(const void* k_rows, const void* v_rows, int64_t n_rows,
+                             const int32_t* rows, int64_t row0, int layer, int n_heads,
+                             int head_dim, hdf_dtype dtype, void* kv_k, void* kv_vt,
+                             int64_t kv_cap, hdf_stream_t stream);
+hdf_status hdf_kv_read_rows(const void* kv_k, const void* kv_vt, int64_t kv_cap, int layer,
+                            int n_heads, int head_dim, hdf_dtype dtype, const int32_t* rows,
+                            int64_t row0, int64_t n_rows, void* k_rows, void* v_rows,
+                            hdf_stream_t stream);
+
 /* Workspace bytes hdf_draft_block needs for these sizes (0 on invalid arguments). */
 size_t hdf_draft_block_workspace(const hdf_drafter* w, int n_seq, int B, int64_t n_new,
                                  int max_ctx);
@@ -378,7 +403,7 @@ hdf_status hdf_accept_sample(const int32_t* draft, int draft_stride, const float
 /* ------------------------------------------------------------------------------
  * 6. LM-head KL distillation forward (Sec. 2.4, a training-side objective).
  *
- * For block s anchored at position a, draft position k = 1..P (the token at a+k) is
+ * Block s with its anchor at index a: slot k = 1..P targets token index a+k and is
  * supervised by the teacher t_k = LMHead(h_{a+k-1}), h the mean of the target's m
  * residual paths at that position and LMHead(h) = (RMSNorm(h) * gamma) W_lm^T:
  *     kl[s][k-1] = KL(softmax(t_k / T) || softmax(z_k / T)),  z_k the draft logits of slot k

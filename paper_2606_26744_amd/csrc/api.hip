@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include <atomic>
+#include <initializer_list>
 #include <mutex>
 
 #include "../../include/hdf.h"
@@ -434,6 +435,71 @@ size_t hdf_kv_cache_bytes(const hdf_drafter* w, int64_t kv_cap) {
   if (w == nullptr || kv_cap < 0) return 0;
   const size_t el = w->dtype == HDF_BF16 ? 2 : 4;
   return size_t(w->n_layers) * size_t(w->d) * size_t(kv_cap) * el;
+}
+
+static hdf_status kv_rows_check(const char* fn, const void* kc, const void* vc, int64_t kv_cap,
+                                int layer, int n_heads, int head_dim, hdf_dtype dtype,
+                                const int32_t* rows, int64_t row0, int64_t n_rows,
+                                const void* krows, const void* vrows) {
+  if (dtype != HDF_F32 && dtype != HDF_BF16) return fail(HDF_E_INVALID, "%s: bad dtype", fn);
+  if (n_rows < 0 || row0 < 0 || layer < 0 || n_heads < 1)
+    return fail(HDF_E_INVALID, "%s: negative size, row or layer", fn);
+  if (head_dim != 64 && head_dim != 128)
+    return fail(HDF_E_UNSUPPORTED, "%s: head_dim %d not in {64, 128}", fn, head_dim);
+  if (kv_cap <= 0 || kv_cap % 64 != 0)
+    return fail(HDF_E_INVALID, "%s: kv_cap must be a positive multiple of 64", fn);
+  if (kv_cap > INT32_MAX || n_rows > INT32_MAX)
+    return fail(HDF_E_UNSUPPORTED, "%s: rows beyond 2^31 - 1", fn);
+  if (rows == nullptr && row0 + n_rows > kv_cap)
+    return fail(HDF_E_INVALID, "%s: rows row0..row0+n_rows-1 leave the cache (kv_cap %lld)", fn,
+                static_cast<long long>(kv_cap));
+  if (n_rows == 0) return HDF_OK;
+  const bool kp = kc != nullptr && krows != nullptr, vp = vc != nullptr && vrows != nullptr;
+  if (!kp && !vp) return fail(HDF_E_INVALID, "%s: neither a key nor a value pair given", fn);
+  if ((kc == nullptr) != (krows == nullptr) || (vc == nullptr) != (vrows == nullptr))
+    return fail(HDF_E_INVALID, "%s: a cache array without its rows (or the reverse)", fn);
+  for (const void* p : {kc, vc, krows, vrows})
+    if (p != nullptr && !aligned16(p))
+      return fail(HDF_E_INVALID, "%s: tensors must be 16-byte aligned", fn);
+  return HDF_OK;
+}
+
+hdf_status hdf_kv_write_rows(const void* k_rows, const void* v_rows, int64_t n_rows,
+                             const int32_t* rows, int64_t row0, int layer, int n_heads,
+                             int head_dim, hdf_dtype dtype, void* kv_k, void* kv_vt,
+                             int64_t kv_cap, hdf_stream_t stream) {
+  const hdf_status st = kv_rows_check("kv_write_rows", kv_k, kv_vt, kv_cap, layer, n_heads,
+                                      head_dim, dtype, rows, row0, n_rows, k_rows, v_rows);
+  if (st != HDF_OK || n_rows == 0) return st == HDF_OK ? ok() : st;
+  const size_t el = dtype == HDF_BF16 ? 2 : 4;
+  const size_t layer_bytes = size_t(n_heads) * size_t(kv_cap) * head_dim * el;
+  char* kc = kv_k ? static_cast<char*>(kv_k) + size_t(layer) * layer_bytes : nullptr;
+  char* vc = kv_vt ? static_cast<char*>(kv_vt) + size_t(layer) * layer_bytes : nullptr;
+  const hipError_t e = hdf::launch_kv_rows(dtype == HDF_BF16, true, kc, vc, kv_cap,
+                                           const_cast<void*>(k_rows), const_cast<void*>(v_rows),
+                                           n_rows, rows, row0, n_heads, head_dim,
+                                           reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "kv_write_rows launch");
+  return ok();
+}
+
+hdf_status hdf_kv_read_rows(const void* kv_k, const void* kv_vt, int64_t kv_cap, int layer,
+                            int n_heads, int head_dim, hdf_dtype dtype, const int32_t* rows,
+                            int64_t row0, int64_t n_rows, void* k_rows, void* v_rows,
+                            hdf_stream_t stream) {
+  const hdf_status st = kv_rows_check("kv_read_rows", kv_k, kv_vt, kv_cap, layer, n_heads,
+                                      head_dim, dtype, rows, row0, n_rows, k_rows, v_rows);
+  if (st != HDF_OK || n_rows == 0) return st == HDF_OK ? ok() : st;
+  const size_t el = dtype == HDF_BF16 ? 2 : 4;
+  const size_t layer_bytes = size_t(n_heads) * size_t(kv_cap) * head_dim * el;
+  const char* kc = kv_k ? static_cast<const char*>(kv_k) + size_t(layer) * layer_bytes : nullptr;
+  const char* vc = kv_vt ? static_cast<const char*>(kv_vt) + size_t(layer) * layer_bytes : nullptr;
+  const hipError_t e = hdf::launch_kv_rows(dtype == HDF_BF16, false, const_cast<char*>(kc),
+                                           const_cast<char*>(vc), kv_cap, k_rows, v_rows, n_rows,
+                                           rows, row0, n_heads, head_dim,
+                                           reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "kv_read_rows launch");
+  return ok();
 }
 
 size_t hdf_draft_block_workspace(const hdf_drafter* w, int n_seq, int B, int64_t n_new,

@@ -179,6 +179,14 @@ hipError_t launch_kl_forward(bool bf16, const void* H_pos, int m, const float* g
                              const int32_t* labels, int n_seq, int P, float T, float alpha,
                              float* kl, float* ce, float* loss, void* ws, hipStream_t s);
 
+// ---------------------------------------------------------------- cache rows (kv_rows.hip)
+// write: k/v rows [n][nh*hd] -> cache tiles of one layer (kc, vc); otherwise the reverse.
+// Cache row of input row i: rows[i], or row0 + i when rows is NULL; rows outside [0, cap)
+// are skipped (write) or read as zeros.  A NULL pair (kc/krows or vc/vrows) is skipped.
+hipError_t launch_kv_rows(bool bf16, bool write, void* kc, void* vc, int64_t cap, void* krows,
+                          void* vrows, int64_t n, const int32_t* rows, int64_t row0, int nh,
+                          int hd, hipStream_t s);
+
 // ---------------------------------------------------------------- attention (attention.hip)
 struct AttnArgs {
   const void* q;             // [n_seq][nh][B][hd]

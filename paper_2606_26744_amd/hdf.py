@@ -28,7 +28,7 @@ EXPORTS = ("hdf_last_error", "hdf_version", "hdf_hc_reduce", "hdf_rope_table",
            "hdf_lm_head_workspace", "hdf_lm_head_argmax", "hdf_accept",
            "hdf_sample_workspace", "hdf_sample_tokens", "hdf_accept_sample_workspace",
            "hdf_accept_sample", "hdf_kl_forward_workspace", "hdf_kl_forward",
-           "hdf_advance_context")
+           "hdf_advance_context", "hdf_kv_write_rows", "hdf_kv_read_rows")
 
 
 class HdfError(RuntimeError):
@@ -92,6 +92,10 @@ def lib() -> ctypes.CDLL:
     L.hdf_draft_block_paged.restype = _I
     L.hdf_draft_block_paged.argtypes = [ctypes.POINTER(Drafter), _I, _I, _P, _I, _P, _P, _P, _I64,
                                         _P, _I, _P, _P, _I64, _P, _P, _P, _SZ, _P]
+    L.hdf_kv_write_rows.restype = _I
+    L.hdf_kv_write_rows.argtypes = [_P, _P, _I64, _P, _I64, _I, _I, _I, _I, _P, _P, _I64, _P]
+    L.hdf_kv_read_rows.restype = _I
+    L.hdf_kv_read_rows.argtypes = [_P, _P, _I64, _I, _I, _I, _I, _P, _I64, _I64, _P, _P, _P]
     L.hdf_advance_context.restype = _I
     L.hdf_advance_context.argtypes = [_I, _P, _P, _P, _P]
     L.hdf_fc_reduce_workspace.restype = _SZ
@@ -484,88 +488,89 @@ class DrafterHandle:
         return hidden
 
 
-_KV_PERM = {}
+def _kv_dims(kv_k: torch.Tensor):
+    """(n_layers, n_heads, head_dim, kv_cap) of a cache tensor [L][nh][cap/64][64*hd]."""
+    L, nh, tiles, tsz = kv_k.shape
+    return L, nh, tsz // 64, tiles * 64
 
 
-def _kv_perm(hd: int, device):
-    """Offsets of (row r, dim i) inside a 64-row cache tile for keys and for values
-    (the library's tile layout, see hdf.h): two [64, hd] int64 tensors."""
-    key = (hd, str(device))
-    if key not in _KV_PERM:
-        r = torch.arange(64).view(64, 1)
-        i = torch.arange(hd).view(1, hd)
-        rr = r % 32
-        st = 2 * (r // 32) + (rr // 4) % 2
-        ql = 4 * (rr // 8) + rr % 4
-        k_off = ((st * (hd // 32) + i // 32) * 64 + ((i // 8) % 4) * 16 + ql) * 8 + i % 8
-        v_off = (((r // 32) * (hd // 16) + i // 16) * 64 + ((r // 8) % 4) * 16 + i % 16) * 8 + r % 8
-        _KV_PERM[key] = (k_off.to(device), v_off.to(device))
-    return _KV_PERM[key]
+def kv_write_rows(kv_k: torch.Tensor, kv_vt: torch.Tensor, layer: int, k_rows: torch.Tensor,
+                  v_rows: torch.Tensor, *, row0: int = 0, rows: Optional[torch.Tensor] = None,
+                  stream=None):
+    """hdf_kv_write_rows: row i of k_rows / v_rows [n, nh*hd] into cache row rows[i] (int32
+    device tensor) or row0 + i of one layer.  Either k_rows or v_rows may be None."""
+    L, nh, hd, cap = _kv_dims(kv_k)
+    src = k_rows if k_rows is not None else v_rows
+    n = src.shape[0]
+    if not 0 <= layer < L:
+        raise ValueError(f"layer {layer} outside [0, {L})")
+    if rows is not None and (rows.dtype != torch.int32 or rows.numel() != n):
+        raise ValueError("rows must be an int32 tensor with one entry per row")
+    _dev(kv_k, kv_vt, k_rows, v_rows, rows)
+    _check(lib().hdf_kv_write_rows(_ptr(k_rows), _ptr(v_rows), n, _ptr(rows), row0, layer, nh, hd,
+                                   _dt(kv_k), _ptr(kv_k) if k_rows is not None else None,
+                                   _ptr(kv_vt) if v_rows is not None else None, cap,
+                                   _stream(stream)))
+
+
+def kv_read_rows(kv_k: torch.Tensor, kv_vt: torch.Tensor, layer: int, n: int, *, row0: int = 0,
+                 rows: Optional[torch.Tensor] = None, stream=None):
+    """hdf_kv_read_rows: cache rows rows[i] (or row0 + i), i < n, of one layer as row-major
+    (keys [n, nh*hd], values [n, nh*hd])."""
+    L, nh, hd, cap = _kv_dims(kv_k)
+    if not 0 <= layer < L:
+        raise ValueError(f"layer {layer} outside [0, {L})")
+    if rows is not None and (rows.dtype != torch.int32 or rows.numel() != n):
+        raise ValueError("rows must be an int32 tensor with one entry per row")
+    k = torch.empty((n, nh * hd), dtype=kv_k.dtype, device=kv_k.device)
+    v = torch.empty_like(k)
+    _dev(kv_k, kv_vt, rows)
+    _check(lib().hdf_kv_read_rows(_ptr(kv_k), _ptr(kv_vt), cap, layer, nh, hd, _dt(kv_k),
+                                  _ptr(rows), row0, n, _ptr(k), _ptr(v), _stream(stream)))
+    return k, v
 
 
 def write_kv_rows(kv_k: torch.Tensor, kv_vt: torch.Tensor, layer: int, row0: int,
                   k_rows: torch.Tensor, v_rows: torch.Tensor):
-    """Copies keys/values of consecutive positions [n, nh*hd] into cache rows row0..row0+n-1
-    (row0 a multiple of 64) of one layer.  Layout conversion only; the rest of the last
-    64-row tile is zero-filled."""
-    n = k_rows.shape[0]
-    if n == 0:
+    """Keys/values of consecutive positions [n, nh*hd] into cache rows row0..row0+n-1 of
+    one layer (hdf_kv_write_rows)."""
+    if k_rows.shape[0] == 0:
         return
-    _, nh, tiles, tsz = kv_k.shape
-    hd = tsz // 64
-    if row0 % 64:
-        raise ValueError("row0 must be a multiple of 64")
-    n64 = (n + 63) // 64
-    t0 = row0 // 64
-    k_off, v_off = _kv_perm(hd, kv_k.device)
-    for src, dst, off in ((k_rows, kv_k, k_off), (v_rows, kv_vt, v_off)):
-        rows = torch.zeros((n64 * 64, nh, hd), dtype=src.dtype, device=src.device)
-        rows[:n] = src.view(n, nh, hd)
-        t = rows.view(n64, 64, nh, hd).permute(2, 0, 1, 3).reshape(nh, n64, 64 * hd)
-        out = torch.empty_like(t)
-        out.scatter_(2, off.reshape(1, 1, -1).expand(nh, n64, -1), t)
-        dst[layer, :, t0:t0 + n64] = out
+    kv_write_rows(kv_k, kv_vt, layer, k_rows.contiguous(), v_rows.contiguous(), row0=row0)
 
 
 def read_kv_rows(kv_k: torch.Tensor, kv_vt: torch.Tensor, layer: int, row0: int, n: int):
     """Keys/values of cache rows row0..row0+n-1 of one layer as [n, nh*hd] tensors."""
-    _, nh, tiles, tsz = kv_k.shape
-    hd = tsz // 64
-    t_lo, t_hi = row0 // 64, (row0 + n + 63) // 64
-    k_off, v_off = _kv_perm(hd, kv_k.device)
-    res = []
-    for src, off in ((kv_k, k_off), (kv_vt, v_off)):
-        t = src[layer, :, t_lo:t_hi]                                   # [nh][tiles][64*hd]
-        g = torch.gather(t, 2, off.reshape(1, 1, -1).expand(nh, t_hi - t_lo, -1))
-        rows = g.view(nh, t_hi - t_lo, 64, hd).permute(1, 2, 0, 3).reshape((t_hi - t_lo) * 64, nh * hd)
-        off0 = row0 - t_lo * 64
-        res.append(rows[off0:off0 + n].contiguous())
-    return res[0], res[1]
+    return kv_read_rows(kv_k, kv_vt, layer, n, row0=row0)
+
+
+def paged_rows(pages: Sequence[int], n: int, device) -> torch.Tensor:
+    """Cache rows of positions 0..n-1 of a sequence stored in `pages` (position p is row
+    p % 64 of page pages[p // 64]), as an int32 device tensor."""
+    pg = torch.as_tensor(list(pages)[:(n + 63) // 64], dtype=torch.int64)
+    p = torch.arange(n, dtype=torch.int64)
+    return (pg[p // 64] * 64 + p % 64).to(torch.int32).to(device)
 
 
 def write_kv_rows_paged(kv_k: torch.Tensor, kv_vt: torch.Tensor, layer: int, pages: Sequence[int],
                         k_rows: torch.Tensor, v_rows: torch.Tensor):
-    """Copies keys/values of positions 0..n-1 of one sequence into its pages (position i
-    goes to row i%64 of page pages[i//64]) of one layer.  Layout conversion only."""
+    """Keys/values of positions 0..n-1 of one sequence into its pages (position i goes to
+    row i%64 of page pages[i//64]) of one layer (hdf_kv_write_rows with a row list)."""
     n = k_rows.shape[0]
-    for j in range((n + 63) // 64):
-        lo, hi = 64 * j, min(n, 64 * j + 64)
-        write_kv_rows(kv_k, kv_vt, layer, int(pages[j]) * 64, k_rows[lo:hi], v_rows[lo:hi])
+    if n == 0:
+        return
+    kv_write_rows(kv_k, kv_vt, layer, k_rows.contiguous(), v_rows.contiguous(),
+                  rows=paged_rows(pages, n, kv_k.device))
 
 
 def read_kv_rows_paged(kv_k: torch.Tensor, kv_vt: torch.Tensor, layer: int, pages: Sequence[int],
                        n: int):
     """Keys/values of positions 0..n-1 of one sequence, stored in `pages`, as [n, nh*hd]."""
-    ks, vs = [], []
-    for j in range((n + 63) // 64):
-        k, v = read_kv_rows(kv_k, kv_vt, layer, int(pages[j]) * 64, min(64, n - 64 * j))
-        ks.append(k)
-        vs.append(v)
-    if not ks:
+    if n == 0:
         d = kv_k.shape[1] * (kv_k.shape[3] // 64)
         e = torch.empty((0, d), dtype=kv_k.dtype, device=kv_k.device)
         return e, e.clone()
-    return torch.cat(ks), torch.cat(vs)
+    return kv_read_rows(kv_k, kv_vt, layer, n, rows=paged_rows(pages, n, kv_k.device))
 
 
 def kv_slot_offsets(ctx_lens: Sequence[int]) -> list:

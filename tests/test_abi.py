@@ -98,25 +98,31 @@ def test_pack_weight_validation():
     assert _status(L.hdf_pack_weight(fake, ctypes.c_void_p(8192), 70, 48, 5, None)) == "HDF_E_INVALID"
 
 
-def test_kv_tile_layout_roundtrip():
-    """The cache tile layout is a permutation of each 64-row tile, and writing rows then
-    reading them back returns them (keys and values), for both head widths."""
-    import torch
-    for hd in (64, 128):
-        k_off, v_off = hdf._kv_perm(hd, "cpu")
-        for off in (k_off, v_off):
-            assert torch.equal(torch.sort(off.reshape(-1)).values, torch.arange(64 * hd))
-        nh, n, row0 = 3, 100, 64
-        kv_k = torch.zeros((1, nh, 4, 64 * hd))
-        kv_vt = torch.zeros((1, nh, 4, 64 * hd))
-        k = torch.randn(n, nh * hd)
-        v = torch.randn(n, nh * hd)
-        hdf.write_kv_rows(kv_k, kv_vt, 0, row0, k, v)
-        k2, v2 = hdf.read_kv_rows(kv_k, kv_vt, 0, row0, n)
-        assert torch.equal(k2, k) and torch.equal(v2, v)
-        # key (row r, dim i) of head h sits at kv_k[0, h, tile, k_off[r, i]]
-        assert kv_k[0, 1, 1, k_off[5, 7]] == k[5, hd + 7]
-        assert kv_vt[0, 2, 2, v_off[3, hd - 1]] == v[64 + 3, 2 * hd + hd - 1]
+def test_kv_rows_validation():
+    """hdf_kv_write_rows / hdf_kv_read_rows reject bad sizes, layouts and pointers on the
+    host; n_rows = 0 is a no-op."""
+    L = hdf.lib()
+    f = ctypes.c_void_p(4096)
+
+    def w(n=10, rows=None, row0=0, layer=0, nh=2, hd=64, dt=1, kc=f, vc=f, cap=128, k=f, v=f):
+        return _status(L.hdf_kv_write_rows(k, v, n, rows, row0, layer, nh, hd, dt, kc, vc, cap,
+                                           None))
+
+    def r(n=10, rows=None, row0=0, layer=0, nh=2, hd=64, dt=1, kc=f, vc=f, cap=128, k=f, v=f):
+        return _status(L.hdf_kv_read_rows(kc, vc, cap, layer, nh, hd, dt, rows, row0, n, k, v,
+                                          None))
+    for call in (w, r):
+        assert call(n=-1) == "HDF_E_INVALID"
+        assert call(layer=-1) == "HDF_E_INVALID"
+        assert call(hd=96) == "HDF_E_UNSUPPORTED"
+        assert call(cap=100) == "HDF_E_INVALID"              # not a multiple of 64
+        assert call(cap=0) == "HDF_E_INVALID"
+        assert call(dt=3) == "HDF_E_INVALID"
+        assert call(row0=120) == "HDF_E_INVALID"             # rows 120..129 leave a 128-row cache
+        assert call(kc=None, vc=None) == "HDF_E_INVALID"     # nothing to copy
+        assert call(k=None) == "HDF_E_INVALID"               # a cache array without rows
+        assert call(kc=ctypes.c_void_p(4100)) == "HDF_E_INVALID"   # misaligned
+        assert call(n=0, kc=None, vc=None, k=None, v=None) == "HDF_OK"
 
 
 def _fake_drafter(L_layers=1, d=256, nh=4, hd=64):
