@@ -314,6 +314,22 @@ hdf_status hdf_lm_head_argmax(const void* hidden, const void* W_lm, int64_t M, i
                               hdf_dtype dtype, int32_t* argmax, float* max_logit, float* logits,
                               void* ws, size_t ws_bytes, hdf_stream_t stream);
 
+/* hdf_lm_head_argmax for callers that cannot allocate device memory (code under HIP
+ * graph capture, serving loops or harnesses that forbid allocation): the same kernels and
+ * results, with no workspace argument.  The per-row argmax keys live in a library-owned
+ * device array of 65536 64-bit words (512 KiB), one per GPU, held until the process
+ * ends; the call allocates nothing.
+ * Every call on one GPU shares that array and hands it back zeroed: calls that overlap on
+ * one GPU (other streams, other threads) race and must be serialised by the caller.  The
+ * first call on each GPU sets the array up (finds its address, clears it and waits for the
+ * clear on `stream`), so it must not be made while `stream` is being captured
+ * (HDF_E_INVALID).
+ * Arguments, outputs and limits as hdf_lm_head_argmax, and M <= 65536
+ * (HDF_E_UNSUPPORTED above). */
+hdf_status hdf_lm_head_argmax_noalloc(const void* hidden, const void* W_lm, int64_t M, int d,
+                                      int vocab, hdf_dtype dtype, int32_t* argmax,
+                                      float* max_logit, float* logits, hdf_stream_t stream);
+
 /* ------------------------------------------------------------------------------
  * 4. Greedy acceptance (Sec. 1: the target keeps the longest draft prefix that
  * agrees with its own tokens; Sec. 3.4: tau, the mean accepted length).

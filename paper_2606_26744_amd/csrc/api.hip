@@ -802,4 +802,90 @@ hdf_status hdf_lm_head_argmax(const void* hidden, const void* W_lm, int64_t M, i
   return ok();
 }
 
+// ---------------------------------------------------------- LM head without a workspace
+// For callers that cannot allocate: the per-row argmax keys live in this file-scope device
+// array (one copy per GPU, held until the process ends) instead of a workspace.  In host
+// code `scratch` names a host-side stand-in, never the device memory: its device address
+// is looked up once per device (hipGetSymbolAddress) and only that address is used.
+}  // extern "C"
+
+namespace {
+
+constexpr int64_t kNoAllocRows = 65536;   // rows of one call; 512 KiB of keys
+static __device__ __align__(256) unsigned long long scratch[kNoAllocRows];
+
+__global__ void zero_keys_kernel(unsigned long long* keys, int64_t n) {
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * blockDim.x)
+    keys[i] = 0ull;
+}
+
+std::mutex g_noalloc_mu;
+unsigned long long* g_noalloc_keys[64];   // device address of `scratch` per device (set up)
+
+// Device address of this device's `scratch`, set up on first use: address lookup, one
+// clearing pass on `s` and a wait for it, so that every later call (on any stream) finds
+// the keys zero, as the LM-head kernels require.
+hdf_status noalloc_keys(hipStream_t s, unsigned long long** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "lm_head_argmax_noalloc: hipGetDevice");
+  if (dev < 0 || dev >= 64) return fail(HDF_E_UNSUPPORTED, "lm_head_argmax_noalloc: device %d", dev);
+  std::lock_guard<std::mutex> lock(g_noalloc_mu);
+  if (g_noalloc_keys[dev] == nullptr) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    e = hipStreamIsCapturing(s, &cs);
+    if (e != hipSuccess) return hip_fail(e, "lm_head_argmax_noalloc: hipStreamIsCapturing");
+    if (cs != hipStreamCaptureStatusNone)
+      return fail(HDF_E_INVALID,
+                  "lm_head_argmax_noalloc: the first call on a device sets up its key array "
+                  "and must not be captured");
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol,
+                      "lm_head_argmax_noalloc: hipGetSymbolAddress");
+    unsigned long long* keys = static_cast<unsigned long long*>(p);
+    hipLaunchKernelGGL(zero_keys_kernel, dim3(256), dim3(256), 0, s, keys, kNoAllocRows);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "lm_head_argmax_noalloc: clearing the keys");
+    g_noalloc_keys[dev] = keys;
+  }
+  *out = g_noalloc_keys[dev];
+  return HDF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+hdf_status hdf_lm_head_argmax_noalloc(const void* hidden, const void* W_lm, int64_t M, int d,
+                                      int vocab, hdf_dtype dtype, int32_t* argmax,
+                                      float* max_logit, float* logits, hdf_stream_t stream) {
+  if (dtype != HDF_F32 && dtype != HDF_BF16)
+    return fail(HDF_E_INVALID, "lm_head_argmax_noalloc: bad dtype");
+  if (M < 0) return fail(HDF_E_INVALID, "lm_head_argmax_noalloc: M < 0");
+  if (d <= 0 || d % 64 != 0)
+    return fail(HDF_E_INVALID, "lm_head_argmax_noalloc: d=%d not a positive multiple of 64", d);
+  if (vocab < 1) return fail(HDF_E_INVALID, "lm_head_argmax_noalloc: vocab < 1");
+  if (M > kNoAllocRows)
+    return fail(HDF_E_UNSUPPORTED, "lm_head_argmax_noalloc: M=%lld above %lld rows",
+                static_cast<long long>(M), static_cast<long long>(kNoAllocRows));
+  if (M == 0) return ok();
+  if (hidden == nullptr || W_lm == nullptr || argmax == nullptr)
+    return fail(HDF_E_INVALID, "lm_head_argmax_noalloc: null pointer");
+  if (!aligned16(hidden) || !aligned16(W_lm))
+    return fail(HDF_E_INVALID, "lm_head_argmax_noalloc: hidden and W_lm must be 16-byte aligned");
+  const hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  unsigned long long* keys = nullptr;
+  const hdf_status st = noalloc_keys(s, &keys);
+  if (st != HDF_OK) return st;
+  // The same kernels as hdf_lm_head_argmax; its finalize pass hands the keys back zeroed.
+  hipError_t e = hdf::launch_lm_head(dtype == HDF_BF16, hidden, W_lm, M, d, vocab, keys, argmax,
+                                     max_logit, logits, s);
+  if (e != hipSuccess) return hip_fail(e, "lm_head_argmax_noalloc launch");
+  return ok();
+}
+
 }  // extern "C"

@@ -28,7 +28,8 @@ EXPORTS = ("hdf_last_error", "hdf_version", "hdf_hc_reduce", "hdf_rope_table",
            "hdf_lm_head_workspace", "hdf_lm_head_argmax", "hdf_accept",
            "hdf_sample_workspace", "hdf_sample_tokens", "hdf_accept_sample_workspace",
            "hdf_accept_sample", "hdf_kl_forward_workspace", "hdf_kl_forward",
-           "hdf_advance_context", "hdf_kv_write_rows", "hdf_kv_read_rows")
+           "hdf_advance_context", "hdf_kv_write_rows", "hdf_kv_read_rows",
+           "hdf_lm_head_argmax_noalloc")
 
 
 class HdfError(RuntimeError):
@@ -106,6 +107,8 @@ def lib() -> ctypes.CDLL:
     L.hdf_lm_head_workspace.argtypes = [_I64, _I]
     L.hdf_lm_head_argmax.restype = _I
     L.hdf_lm_head_argmax.argtypes = [_P, _P, _I64, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]
+    L.hdf_lm_head_argmax_noalloc.restype = _I
+    L.hdf_lm_head_argmax_noalloc.argtypes = [_P, _P, _I64, _I, _I, _I, _P, _P, _P, _P]
     L.hdf_accept.restype = _I
     L.hdf_accept.argtypes = [_P, _I, _P, _I, _I, _P, _P, _P, _P, _P]
     _U64 = ctypes.c_uint64
