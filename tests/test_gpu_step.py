@@ -66,7 +66,7 @@ def _step_case(wl, ctx, new, *, sub=0, uniform_targets=False):
         rng = np.random.default_rng([wl.seed, 99, sub])
         targets = rng.integers(0, V, (n_seq, B)).astype(np.int32)
     else:
-        targets = synth.make_targets(drafts_ref, wl.match_p or [0.8] * n_seq, V, seed=wl.seed,
+        targets = synth.make_targets(drafts_ref, (wl.match_p or [0.8] * n_seq)[:n_seq], V, seed=wl.seed,
                                      sub=sub)
     near = margin.reshape(n_seq, B)[:, 1:] < MARGIN
     low = np.argmin(lg_ref.reshape(n_seq, B, V)[:, 1:], axis=2).astype(np.int32)
