@@ -43,9 +43,17 @@ def parse():
     ap.add_argument("--no-reducer-stress", action="store_true")
     ap.add_argument("--no-m-sweep", action="store_true")
     ap.add_argument("--ragged", action="store_true",
-                    help="also time the 64-sequence ragged decode workload")
+                    help="(default; kept for old command lines) time the 64-sequence ragged "
+                         "decode workload")
+    ap.add_argument("--no-ragged", action="store_true",
+                    help="skip the 64-sequence ragged decode workload")
     ap.add_argument("--cold", action="store_true",
                     help="also time the cold step (every context row reduced and projected)")
+    ap.add_argument("--ragged-cold", action="store_true",
+                    help="also time the cold step of the ragged workload (about 540K context "
+                         "rows reduced and projected)")
+    ap.add_argument("--no-cold-cache", action="store_true",
+                    help="skip the headline step timed with the caches flushed before each step")
     ap.add_argument("--decode", type=int, default=0, metavar="R",
                     help="also time R chained rounds of the paged decode loop (8 sequences "
                          "from 2048 positions, n+1 committed positions appended per round)")
@@ -72,8 +80,9 @@ def build_workload(torch, synth, hdf, wl=None):
     from paper_2606_26744_amd.step import StepBuffers
     wl = wl or synth.drafter_full()
     dr = wl.drafter
-    n_seq, B, n_s = wl.n_seq, wl.block, wl.new_rows
+    n_seq, B = wl.n_seq, wl.block
     lens = [int(t) for t in wl.ctx_lens]
+    news = lens if wl.cold else [wl.new_rows] * n_seq      # rows reduced/projected per step
     T = max(lens)
     dev = "cuda"
     w = synth.drafter_weights(wl, device=dev)
@@ -83,18 +92,24 @@ def build_workload(torch, synth, hdf, wl=None):
     offs = hdf.kv_slot_offsets(lens)
     kv_k, kv_vt = h.alloc_kv(offs[-1])
     for s in range(n_seq):          # rows of earlier rounds, already in the cache
+        if lens[s] - news[s] <= 0:
+            continue
         for l in range(dr.n_layers):
-            k, v = synth.kv_prefix(wl, lens[s] - n_s, l, device=dev, sub=s)
+            k, v = synth.kv_prefix(wl, lens[s] - news[s], l, device=dev, sub=s)
             hdf.write_kv_rows(kv_k, kv_vt, l, offs[s], k, v)
             del k, v
-    red = synth.reducer_inputs(wl, n_seq * n_s, device=dev)
+    n_new = sum(news)
+    red = synth.reducer_inputs(wl, n_new, device=dev)
     i32 = dict(dtype=torch.int32, device=dev)
+    new_offsets = [0]
+    for n in news:
+        new_offsets.append(new_offsets[-1] + n)
     args = dict(H_new=red["H"], W_g=red["W_g"], b_g=red["b_g"],
-                new_offsets=torch.arange(0, n_seq * n_s + 1, n_s, **i32),
+                new_offsets=torch.tensor(new_offsets, **i32),
                 ctx_len=torch.tensor(lens, **i32), max_ctx=T,
                 kv_offsets=torch.tensor(offs, **i32), kv_k=kv_k, kv_vt=kv_vt,
                 tokens=synth.block_tokens(wl, device=dev))
-    bufs = StepBuffers(h, n_seq, B, n_seq * n_s, T, wl.m)
+    bufs = StepBuffers(h, n_seq, B, n_new, T, wl.m)
     return wl, h, bufs, args, red, w, offs
 
 
@@ -109,9 +124,11 @@ def step_targets(torch, synth, hdf, wl, h, bufs, args):
                                               seed=wl.seed)).cuda()
 
 
-def ragged_leg(torch, synth, hdf, steps, warmup, wl=None):
+def ragged_leg(torch, synth, hdf, steps, warmup, wl=None, cpu_seqs=None):
     """A further step workload, timed like the headline step: by default the batched ragged
-    decode workload (64 sequences, contexts U[1024, 16384]), warm-step blocks/s."""
+    decode workload (64 sequences, contexts U[1024, 16384]), warm-step blocks/s.  With
+    cpu_seqs, the oracle's time on those sequences of the same step is reported beside it
+    (a bounded sample of the workload, scaled to blocks/s)."""
     from paper_2606_26744_amd.step import drafter_step
     wl, h, bufs, args, red, w, offs = build_workload(torch, synth, hdf,
                                                      wl or synth.ragged_decode())
@@ -131,6 +148,11 @@ def ragged_leg(torch, synth, hdf, steps, warmup, wl=None):
            "context_min": int(min(wl.ctx_lens)), "context_max": int(max(wl.ctx_lens)),
            "blocks_per_s": round(wl.n_seq / (ms * 1e-3), 1), "ms_per_step": round(ms, 4),
            "steps": steps, "mean_accept_len": round(float(acc.mean()), 3)}
+    if wl.cold:
+        res["context_rows_projected"] = int(sum(wl.ctx_lens))
+    if cpu_seqs is not None:
+        res["cpu_baseline"] = cpu_baseline(torch, synth, wl, h, w, red, args, offs, seqs=cpu_seqs,
+                                           budget_s=10.0)
     del wl, h, bufs, args, red, w
     torch.cuda.empty_cache()
     return res
@@ -423,8 +445,28 @@ def _kernel_source_sha():
     return hashlib.sha256(data.encode()).hexdigest()[:16]
 
 
-def cpu_baseline(torch, synth, wl, h, w, red, args, offs):
-    """The oracle as it stands, on the whole step (all eight sequences)."""
+def _blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        return len(os.sched_getaffinity(0))
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(torch, synth, wl, h, w, red, args, offs, seqs=None, budget_s=10.0):
+    """The oracle as it stands on the whole step of sequences `seqs` (default: all of
+    them), blocks/s; the same inputs the GPU step took, the cached rows read back from
+    the GPU's cache.  Repeats for about budget_s seconds (at least twice), median."""
     import numpy as np
     from oracle.accept import accept
     from oracle.drafter import Weights, draft_block
@@ -432,58 +474,152 @@ def cpu_baseline(torch, synth, wl, h, w, red, args, offs):
     from oracle.reducer import hc_reduce
     dr = wl.drafter
     b = synth.to_numpy_bits
-    n_s, T, B = wl.new_rows, wl.ctx_lens[0], wl.block
-    n_seq = wl.n_seq
-    t0 = T - n_s
+    B = wl.block
+    seqs = list(range(wl.n_seq)) if seqs is None else list(seqs)
+    lens = [int(t) for t in wl.ctx_lens]
+    news = lens if wl.cold else [wl.new_rows] * wl.n_seq
+    no = np.concatenate([[0], np.cumsum(news)])
     wb = {k: ([b(x) for x in v] if isinstance(v, list) else b(v)) for k, v in w.items()}
     W = Weights(wb, d=dr.d, n_layers=dr.n_layers, n_heads=dr.n_heads, head_dim=dr.head_dim,
                 d_ff=dr.d_ff, vocab=dr.vocab, eps=dr.eps, rope_theta=dr.rope_theta, dtype="bf16")
     from paper_2606_26744_amd import hdf
     pre = []
-    for s in range(n_seq):
+    for s in seqs:
+        t0 = lens[s] - news[s]
         per = []
         for l in range(dr.n_layers):
             k, v = hdf.read_kv_rows(args["kv_k"], args["kv_vt"], l, offs[s], t0)
             per.append((b(k), b(v)))
         pre.append(per)
-    H = b(red["H"])
+    H = [b(red["H"][int(no[s]):int(no[s + 1])]) for s in seqs]
     Wg, bg = b(red["W_g"]), b(red["b_g"])
-    toks = b(args["tokens"])
+    toks = b(args["tokens"])[seqs]
+    p = [wl.match_p[s] for s in seqs]
     times = []
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        threads = len(os.sched_getaffinity(0))
-    budget_s = 10.0   # about ten seconds of CPU work in total, at least two runs
     t_total = 0.0
     while len(times) < 2 or (t_total < budget_s and len(times) < 20):
         t_start = time.perf_counter()
-        ys = [hc_reduce(H[s * n_s:(s + 1) * n_s], Wg, bg, dtype="bf16")[0] for s in range(n_seq)]
+        ys = [hc_reduce(Hs, Wg, bg, dtype="bf16")[0] for Hs in H]
         hid = draft_block(W, ys, toks, kv_prefix=pre)
         am, _, _ = lm_head_argmax(hid, W.w_lm)
-        drafts = am.reshape(n_seq, B)[:, 1:]
-        tg = synth.make_targets(drafts, wl.match_p, dr.vocab, seed=wl.seed)
+        drafts = am.reshape(len(seqs), B)[:, 1:]
+        tg = synth.make_targets(drafts, p, dr.vocab, seed=wl.seed)
         accept(drafts, tg)
         times.append(time.perf_counter() - t_start)
         t_total += times[-1]
     t = statistics.median(times)
-    cpu = "unknown"
-    try:
-        for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                cpu = line.split(":", 1)[1].strip()
-                break
-    except OSError:
-        pass
-    return {"value": round(n_seq / t, 4), "unit": "blocks/s", "cores": int(threads),
+    ctx = ("every context row reduced and projected" if wl.cold
+           else f"{news[seqs[0]]} new context rows each reduced and projected")
+    return {"value": round(len(seqs) / t, 4), "unit": "blocks/s", "cores": int(_blas_threads()),
             "kind": "oracle",
-            "sample": f"the whole warm step ({n_seq} sequences: 16 new context rows each "
-                      f"reduced and projected, 2048-position context, B=16, full-vocabulary "
-                      f"argmax, acceptance); median of {len(times)} runs ({t_total:.1f} s in total), "
-                      f"{t:.2f} s per step; "
-                      f"float64 NumPy; host CPU {cpu}; affinity "
-                      f"{len(os.sched_getaffinity(0))} cores"}
+            "sample": f"{wl.name}: the whole step of {len(seqs)} of its {wl.n_seq} sequences "
+                      f"(contexts {[lens[s] for s in seqs]}, {ctx}, B={B}, full-vocabulary "
+                      f"argmax, acceptance); median of {len(times)} runs ({t_total:.1f} s in "
+                      f"total), {t:.2f} s per step; float64 NumPy; host CPU {_cpu_model()}; "
+                      f"affinity {len(os.sched_getaffinity(0))} cores"}
+
+
+def cpu_reducer_baseline(synth, sw, ri, n_sample=2048):
+    """The oracle's gated reducer (Eq. 1, float64 NumPy) on n_sample tokens of the stress
+    shape, with every BLAS thread and with one, as GB/s of the reducer's algorithmic
+    bytes (the same unit as the GPU figure)."""
+    from oracle.reducer import hc_reduce
+    b = synth.to_numpy_bits
+    H = b(ri["H"][:n_sample])
+    Wg, bg = b(ri["W_g"]), b(ri["b_g"])
+    nbytes = n_sample * sw.m * sw.d * 2 + n_sample * sw.d * 2
+    out = {}
+
+    def timed():
+        ts = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            hc_reduce(H, Wg, bg, dtype="bf16")
+            ts.append(time.perf_counter() - t0)
+        return statistics.median(ts)
+
+    t_all = timed()
+    out["all_cores"] = {"value": round(nbytes / t_all / 1e9, 3), "unit": "GB/s",
+                        "cores": int(_blas_threads()), "kind": "oracle",
+                        "sample": f"{n_sample} of the {sw.n_tok} tokens x {sw.m} x {sw.d}, "
+                                  f"median of 3, {t_all * 1e3:.0f} ms each; host CPU "
+                                  f"{_cpu_model()}"}
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(1):
+            t_one = timed()
+        out["single_thread"] = {"value": round(nbytes / t_one / 1e9, 3), "unit": "GB/s",
+                                "cores": 1, "kind": "oracle",
+                                "sample": f"same sample, BLAS limited to one thread, "
+                                          f"{t_one * 1e3:.0f} ms each"}
+    except Exception as e:  # pragma: no cover
+        out["single_thread"] = {"error": str(e)}
+    return out
+
+
+def rw_probe(torch, sw, ri, Y):
+    """The memory-system probe (libhdf_probe.so): the reducer's exact traffic with no
+    arithmetic, read-only and with the 4:1 writes, each the best of the one- and
+    two-token ring depths; GB/s of the bytes moved."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2606_26744_amd", "libhdf_probe.so")
+    if not os.path.exists(path):
+        return {"error": "libhdf_probe.so not built"}
+    L = ctypes.CDLL(path)
+    L.hdf_probe_rw.restype = ctypes.c_int
+    L.hdf_probe_rw.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                               ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                               ctypes.c_void_p, ctypes.c_void_p]
+    sink = torch.zeros(4, dtype=torch.int32, device="cuda")
+    st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    grid = torch.cuda.get_device_properties(0).multi_processor_count
+    H, n, m, d = ri["H"], sw.n_tok, sw.m, sw.d
+    res = {}
+    for write in (0, 1):
+        best = 0.0
+        for pf in (1, 2):
+            def go():
+                rc = L.hdf_probe_rw(ctypes.c_void_p(H.data_ptr()), ctypes.c_void_p(Y.data_ptr()),
+                                    n, m, d, write, pf, grid, ctypes.c_void_p(sink.data_ptr()), st)
+                if rc != 0:
+                    raise RuntimeError(f"hdf_probe_rw returned {rc}")
+            for _ in range(5):
+                go()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(20):
+                go()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) / 20 * 1e3
+            nbytes = n * m * d * 2 + (n * d * 2 if write else 0)
+            best = max(best, nbytes / (us * 1e-6) / 1e9)
+        res["read_4to1_GB/s" if write else "read_only_GB/s"] = round(best, 1)
+    return res
+
+
+def cold_cache_step(torch, h, bufs, args, tg, steps):
+    """The headline step with the caches flushed before every step: a 512 MiB device copy
+    (1 GiB of traffic, well above the 256 MB last-level cache and the L2s) runs ahead of
+    each step, and each step is timed by its own events, so no step finds the previous
+    one's weights in a cache."""
+    from paper_2606_26744_amd.step import drafter_step
+    src = torch.empty(1 << 29, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for i in range(steps):
+        dst.copy_(src)
+        ev[i][0].record()
+        drafter_step(h, bufs, targets=tg, **args)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    ms = statistics.mean(a.elapsed_time(b) for a, b in ev)
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"ms_per_step": round(ms, 4), "steps": steps,
+            "flush": "512 MiB device copy before every step"}
 
 
 def main():
@@ -556,11 +692,17 @@ def main():
     }
     if not a.no_m_sweep:
         res["lm_head_m_sweep"] = lm_head_m_sweep(torch, synth, hdf, h, d)
+    if not a.no_cold_cache:
+        res["cold_cache_step"] = cold_cache_step(torch, h, bufs, args, tg, a.steps)
+        res["cold_cache_step"]["blocks_per_s"] = round(
+            n_seq / (res["cold_cache_step"]["ms_per_step"] * 1e-3), 1)
     if not a.no_reducer_stress:
         sw = synth.reducer_stress()
         ri = synth.reducer_inputs(sw, sw.n_tok, device="cuda")
         Y = torch.empty((sw.n_tok, sw.d), dtype=torch.bfloat16, device="cuda")
-        for _ in range(3):
+        # 30 untimed launches first: under sustained load the GPU needs about 20 ms to
+        # reach its steady memory throughput (the first 20 launches run about 10% slower)
+        for _ in range(30):
             hdf.hc_reduce(ri["H"], ri["W_g"], ri["b_g"], Y=Y)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
@@ -572,10 +714,17 @@ def main():
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) / n_it * 1e3
         rb = sw.n_tok * sw.m * sw.d * 2 + sw.n_tok * sw.d * 2 + sw.m * sw.m * sw.d * 2
+        gbs = rb / (us * 1e-6) / 1e9
         res["reducer_stress"] = {"n_tok": sw.n_tok, "m": sw.m, "d": sw.d, "us": round(us, 1),
-                                 "GB/s": round(rb / (us * 1e-6) / 1e9, 1),
-                                 "frac_hbm": round(rb / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                                 "GB/s": round(gbs, 1),
+                                 "frac_hbm": round(gbs / HBM_PEAK_GBS, 4),
                                  "bytes_per_launch": rb}
+        pr = rw_probe(torch, sw, ri, Y)
+        res["reducer_stress"]["probe"] = pr
+        if "read_4to1_GB/s" in pr:
+            res["reducer_stress"]["frac_of_probe_4to1"] = round(gbs / pr["read_4to1_GB/s"], 4)
+        if not a.no_cpu_baseline:
+            res["reducer_stress"]["cpu_baseline"] = cpu_reducer_baseline(synth, sw, ri)
         del ri, Y
         torch.cuda.empty_cache()
     if a.copy_probe:
@@ -596,11 +745,14 @@ def main():
         res["fc_reducer"] = fc_reducer_leg(torch, synth, hdf)
     if a.blas_ref:
         res["blas_reference"] = blas_reference(torch)
-    if a.ragged or a.cold or a.decode:
+    if not a.no_ragged or a.cold or a.ragged_cold or a.decode:
         del bufs, args
         torch.cuda.empty_cache()
-    if a.ragged:
-        res["ragged_decode"] = ragged_leg(torch, synth, hdf, max(a.steps // 5, 5), 3)
+    if not a.no_ragged:
+        res["ragged_decode"] = ragged_leg(torch, synth, hdf, max(a.steps // 5, 5), 3,
+                                          cpu_seqs=None if a.no_cpu_baseline else [0, 1])
+    if a.ragged_cold:
+        res["ragged_decode_cold"] = ragged_leg(torch, synth, hdf, 3, 1, synth.ragged_decode_cold())
     if a.cold:
         res["drafter_full_cold"] = ragged_leg(torch, synth, hdf, max(a.steps // 5, 5), 3,
                                               synth.drafter_full_cold())

@@ -3,7 +3,9 @@
     python -m paper_2606_26744_amd.build
 
 Compiles every csrc/*.hip to an object with hipcc (in parallel) and links the
-shared library next to this file.  Always recompiles.
+shared library next to this file; also builds libhdf_probe.so from csrc/probe/ (a
+memory-system probe that only bench.py loads, not part of the library).  Always
+recompiles.
 """
 from __future__ import annotations
 
@@ -17,6 +19,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libhdf.so")
+PROBE_OUT = os.path.join(HERE, "libhdf_probe.so")
 ARCH = "gfx950"
 
 # Packed-fp32 instructions are disabled for all device code (they are generated
@@ -63,6 +66,14 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stderr)
     os.replace(tmp, OUT)
+    probes = sorted(glob.glob(os.path.join(CSRC, "probe", "*.hip")))
+    if probes:
+        tmp = PROBE_OUT + ".tmp"
+        cmd = [hipcc, "-shared", *CFLAGS, "-o", tmp, *probes]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError("probe build failed:\n" + r.stderr)
+        os.replace(tmp, PROBE_OUT)
     return OUT
 
 

@@ -106,6 +106,7 @@ class Workload:
     bias_std: float = 0.0                    # gate bias std (0 -> zero bias)
     w_std: float = 0.02
     new_rows: int = 0                        # context rows reduced/projected per step (warm)
+    cold: bool = False                       # every context row reduced/projected per step
 
 
 def tiny_fp32() -> Workload:
@@ -148,6 +149,7 @@ def drafter_full_cold() -> Workload:
     wl = drafter_full()
     wl.name = "drafter_full_cold"
     wl.new_rows = 2048
+    wl.cold = True
     return wl
 
 
@@ -164,6 +166,16 @@ def ragged_decode(n_seq: int = 64) -> Workload:
                     match_p=ps, new_rows=16)
 
 
+def ragged_decode_cold(n_seq: int = 64) -> Workload:
+    """Cold step of the batched ragged workload: the cache starts empty and every context
+    row of the 64 sequences (lengths U[1024, 16384]) is reduced and projected."""
+    wl = ragged_decode(n_seq)
+    wl.name = "ragged_decode_cold"
+    wl.new_rows = 0
+    wl.cold = True
+    return wl
+
+
 WORKLOADS = {
     "tiny_fp32": tiny_fp32,
     "small_bf16": small_bf16,
@@ -171,6 +183,7 @@ WORKLOADS = {
     "drafter_full": drafter_full,
     "drafter_full_cold": drafter_full_cold,
     "ragged_decode": ragged_decode,
+    "ragged_decode_cold": ragged_decode_cold,
 }
 
 

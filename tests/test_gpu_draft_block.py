@@ -141,6 +141,38 @@ def test_ragged_long_contexts_sampled():
     torch.cuda.empty_cache()
 
 
+def test_long_cold_contexts_across_projection_chunks():
+    """Full-size drafter, three cold sequences of 13000, 9000 and 700 positions: 22700
+    context rows projected in one call, in two chunks of the context projection (16384
+    rows, then 6316), the chunk boundary inside sequence 1.  Sampled cache rows of every
+    sequence (each boundary, the chunk boundary and random rows), read back through
+    hdf_kv_read_rows, against oracle.context_kv of the same reduced rows."""
+    wl = synth.drafter_full()
+    ctx = [13000, 9000, 700]
+    print(f"[cold chunks] drafter_full contexts {ctx}", flush=True)
+    case = DraftCase(wl, ctx, ctx, random_norms=False, sub=17)
+    case.run()
+    torch.cuda.synchronize()
+    W = case.oracle_weights()
+    offs = case.kv_offsets.tolist()
+    rng = np.random.default_rng(17)
+    chunk_row = 16384 - ctx[0]            # local row of sequence 1 where the second chunk starts
+    for s, T in enumerate(ctx):
+        pick = {0, 1, 63, 64, T - 2, T - 1}
+        if s == 1:
+            pick |= {chunk_row - 1, chunk_row, chunk_row + 1}
+        pick |= set(rng.choice(T, 120, replace=False).tolist())
+        rows = np.array(sorted(r for r in pick if 0 <= r < T))
+        ys = case.y_rows(s)[rows]
+        ref = context_kv(W, as_f64(ys), rows)
+        k, v = hdf.kv_read_rows(case.kv_k, case.kv_vt, 0, len(rows),
+                                rows=torch.as_tensor(offs[s] + rows, dtype=torch.int32).cuda())
+        assert_bf16_state_close(as_f64(bits(k)), ref[0][0], f"K seq {s}")
+        assert_bf16_state_close(as_f64(bits(v)), ref[0][1], f"V seq {s}")
+    del case
+    torch.cuda.empty_cache()
+
+
 def test_cold_rows_projected_into_the_cache_by_the_gemm_epilogue():
     """8192 cold context rows at head_dim 64 over a paged pool: one K split, so RoPE and
     the cache stores happen in the projection GEMM's epilogue (no fp32 rows in memory)."""
