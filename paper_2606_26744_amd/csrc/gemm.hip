@@ -277,15 +277,20 @@ gemm_bf16_kernel(GemmArgs p) {
         }
       }
     };
-    // Prologue: A(0) into LDS; then A(1..STAGES) and B(0..STAGES-1), interleaved in the
-    // order they are consumed.
+    // Prologue.  The weights do not depend on the previous kernel, so B(0) is issued first
+    // and its HBM latency overlaps the activations' L2 latency (issued after A(0) it came
+    // one L2 round trip later).  Then A(1..STAGES-1) and B(1..STAGES-1) in the order they
+    // are consumed, A(0) into LDS (loads complete in issue order: this waits for B(0) and
+    // A(0) only), and A(STAGES) into the register slot A(0) leaves.
+    load_b(0, rb[0]);
     load_a(0, ra[0]);
-    store_a(ra[0], 0);
 #pragma unroll
-    for (int st = 0; st < STAGES; ++st) {
-      load_a(st + 1, ra[(st + 1) % STAGES]);
+    for (int st = 1; st < STAGES; ++st) {
+      load_a(st, ra[st]);
       load_b(st, rb[st]);
     }
+    store_a(ra[0], 0);
+    load_a(STAGES, ra[0]);
     __syncthreads();
     // Step t (ring slot u = t % STAGES): compute with A(t) in LDS and B(t) in rb[u];
     // move A(t+1) into the other LDS buffer; refill the freed slots with A(t+1+STAGES)
