@@ -651,8 +651,22 @@ static void launch_bf16_partial(const GemmArgs& a, int splits, hipStream_t s) {
                        0, s, a);
 }
 
+// One pass for 128 < M <= 256 rows: every row in one tile (192 or 256 rows), 8 waves of
+// one 32-column block, the weights streamed once (non-temporal).  Two 128-row tiles
+// re-streamed the weights through L2 instead (M = 192: 277 -> 211 us, M = 256: 289 -> 262
+// us).  One column block per wave reads a 1 KB activation fragment per MFMA, which at 256
+// rows is the LDS bandwidth of the CU.
+template <int BM>
+static void launch_bf16_argmax_tall(const GemmArgs& a, hipStream_t s) {
+  constexpr int BN = 32 * 8;
+  const dim3 grid((a.N + BN - 1) / BN, 1, 1), block(8 * 64);
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, 8, 2, kEpiArgmax, 1, true>), grid, block, 0, s, a);
+}
+
 template <int NW, int TN, int STAGES>
 static void launch_bf16_argmax(const GemmArgs& a, hipStream_t s) {
+  if (a.M > 128 && a.M <= 192) return launch_bf16_argmax_tall<192>(a, s);
+  if (a.M > 192 && a.M <= 256) return launch_bf16_argmax_tall<256>(a, s);
   const int BM = a.M <= 64 ? 64 : 128;
   constexpr int BN = 32 * NW * TN;
   const int mt = (a.M + BM - 1) / BM;

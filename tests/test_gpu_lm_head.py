@@ -57,7 +57,8 @@ def test_tiny_fp32():
 
 
 @pytest.mark.parametrize("M,d,V", [(64, 1024, 32000), (1, 1024, 1000), (130, 512, 1000),
-                                   (16, 64, 129)])
+                                   (16, 64, 129), (200, 1024, 32000), (256, 512, 5000),
+                                   (300, 256, 3000)])
 def test_bf16_shapes(M, d, V):
     hid, w = _inputs(M, d, V, "bf16", M + V)
     _check(hid, w)
@@ -95,13 +96,14 @@ def test_ties_take_lowest_index():
     assert lg[0, 17].item() == lg[0, 1200].item() == lg[0, 2999].item()
 
 
-@pytest.mark.parametrize("M", [4, 100, 136])
+@pytest.mark.parametrize("M", [4, 100, 136, 250])
 def test_ties_inside_one_tile_take_lowest_index(M):
     """Tied columns inside one 512-column tile, one pair per row, placed so that each
     level of the tile's (max, lowest index) combine decides one pair: the same lane
     (33 vs 40), the two lane halves (4 vs 8), the two 32-column blocks of a wave (20 vs
     36) and different waves (70 vs 200).  M = 4 runs 64-row tiles, M = 100 one 128-row
-    tile, M = 136 two row tiles (the tie rows repeat in the second one)."""
+    tile, M = 136 and 250 one 192- and one 256-row tile (the tie rows repeat from row
+    130)."""
     d, V = 128, 3000
     pairs = [(4, 8), (33, 40), (20, 36), (70, 200)]      # (expected, tied higher column)
     hid, w = _inputs(M, d, V, "bf16", 65)
