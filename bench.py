@@ -30,8 +30,8 @@ HBM_PEAK_GBS = 8000.0
 # FETCH_SIZE x 1.99997 + WRITE_SIZE x 1.000 KiB, the factors a 2 GiB device copy reads on
 # the same counters.  Valid only for the kernel source it was measured on: reported as
 # null once the code of gemm.hip or common.hpp changes.
-LM_HEAD_TRAFFIC = {"source_sha": "f9e981c56b6b4df9",
-                   "bytes": ((532820.1 + 1.3) * 1.99997 + (253.0 + 2.0) * 1.000) * 1024}
+LM_HEAD_TRAFFIC = {"source_sha": "436f80cdaf898b2f",
+                   "bytes": ((532934.0 + 1.3) * 1.99997 + (253.0 + 2.0) * 1.000) * 1024}
 BF16_PEAK_TFLOPS = 2500.0
 METRIC = "draft blocks/sec at d=4096,B=16,V=129280; reducer HBM GB/s; MFMA util %"
 
@@ -601,6 +601,43 @@ def rw_probe(torch, sw, ri, Y):
     return res
 
 
+def mfma_probe(torch):
+    """The matrix-core probe (libhdf_probe.so): back-to-back v_mfma_f32_32x32x16_bf16 from
+    registers on every SIMD, four waves per SIMD and four accumulator chains per wave, on
+    random operands, no memory traffic: the rate the matrix-core bound kernels can reach
+    at the clock the chip holds under that load (with near-constant operands it holds a
+    higher one: 2.45 PFLOP/s measured, against 1.7-1.8 on random data)."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2606_26744_amd", "libhdf_probe.so")
+    if not os.path.exists(path):
+        return {"error": "libhdf_probe.so not built"}
+    L = ctypes.CDLL(path)
+    L.hdf_probe_mfma.restype = ctypes.c_int
+    L.hdf_probe_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    blocks = 4 * torch.cuda.get_device_properties(0).multi_processor_count
+    sink = torch.zeros(blocks, dtype=torch.float32, device="cuda")
+    st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    iters = 20000
+
+    def go():
+        rc = L.hdf_probe_mfma(blocks, iters, ctypes.c_void_p(sink.data_ptr()), st)
+        if rc != 0:
+            raise RuntimeError(f"hdf_probe_mfma returned {rc}")
+    for _ in range(3):    # about 18 ms: the clock settles under the load first
+        go()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(3):
+        go()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / 3 * 1e3
+    tf = blocks * 4 * 4 * iters * 32768.0 / (us * 1e-6) / 1e12
+    return {"TFLOP/s": round(tf, 1), "frac_of_peak": round(tf / BF16_PEAK_TFLOPS, 4),
+            "us": round(us, 1)}
+
+
 def cold_cache_step(torch, h, bufs, args, tg, steps):
     """The headline step with the caches flushed before every step: a 512 MiB device copy
     (1 GiB of traffic, well above the 256 MB last-level cache and the L2s) runs ahead of
@@ -720,6 +757,11 @@ def main():
     }
     if sweep is not None:
         res["lm_head_m_sweep"] = sweep
+        probe = mfma_probe(torch)
+        res["mfma_probe"] = probe
+        if "TFLOP/s" in probe:
+            for e in sweep:
+                e["frac_of_mfma_probe"] = round(e["TFLOP/s"] / probe["TFLOP/s"], 4)
     if cold is not None:
         res["cold_cache_step"] = cold
         cold["blocks_per_s"] = round(n_seq / (cold["ms_per_step"] * 1e-3), 1)
@@ -772,6 +814,9 @@ def main():
         res["fc_reducer"] = fc_reducer_leg(torch, synth, hdf)
     if a.blas_ref:
         res["blas_reference"] = blas_reference(torch)
+        if "TFLOP/s" in res.get("mfma_probe", {}):
+            for e in res["blas_reference"]:
+                e["frac_of_mfma_probe"] = round(e["TFLOP/s"] / res["mfma_probe"]["TFLOP/s"], 4)
     if not a.no_ragged or a.cold or a.ragged_cold or a.decode:
         del bufs, args
         torch.cuda.empty_cache()
