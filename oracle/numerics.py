@@ -26,7 +26,7 @@ def as_f64(x: np.ndarray) -> np.ndarray:
     x = np.asarray(x)
     if x.dtype == np.uint16:
         return decode_bf16(x)
-    return x.astype(np.float64)
+    return x.astype(np.float64, copy=False)
 
 
 def round_bf16(x: np.ndarray) -> np.ndarray:

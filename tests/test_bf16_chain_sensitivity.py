@@ -22,6 +22,7 @@ import oracle.drafter as od
 import oracle.numerics as nm
 from oracle.drafter import Weights, draft_block
 from oracle.lm_head import lm_head_argmax
+from oracle.numerics import as_f64
 from tests._tol import E2E_LOGIT_ABS, E2E_MARGIN, STATE_RMS_REL
 
 
@@ -79,7 +80,8 @@ def test_bf16_chain_spread_at_full_size(monkeypatch):
     ys = [b(synth.reduced_states(wl, n, sub=s)) for s in range(n_seq)]
     toks = b(synth.block_tokens(wl))
     ref = draft_block(W, ys, toks, kv_prefix=pre)
-    am0, lg0, mg0 = lm_head_argmax(ref, wb["w_lm"])
+    w_lm = as_f64(wb["w_lm"])          # decoded once for both LM-head passes
+    am0, lg0, mg0 = lm_head_argmax(ref, w_lm)
     rng = np.random.default_rng(0)
     orig = nm.store
 
@@ -90,7 +92,7 @@ def test_bf16_chain_spread_at_full_size(monkeypatch):
     monkeypatch.setattr(od, "store", noisy)
     pert = draft_block(W, ys, toks, kv_prefix=pre)
     monkeypatch.setattr(od, "store", orig)
-    am1, lg1, _ = lm_head_argmax(pert, wb["w_lm"])
+    am1, lg1, _ = lm_head_argmax(pert, w_lm)
     d = pert - ref
     changed = np.mean(d != 0)
     rms = np.sqrt((d ** 2).mean(1)) / np.sqrt((ref ** 2).mean(1))
