@@ -647,7 +647,11 @@ static hdf_status draft_block_impl(const hdf_drafter* w, int n_seq, int B, const
   }
 
   const int n_chunks = std::max(1, (max_ctx + P.chunk_len - 1) / P.chunk_len);
+  // With one attention workgroup per (sequence, head), the projection epilogue of the
+  // shared launch runs inside the attention kernel (no launch of its own).
+  const bool fuse_epi = shared && n_chunks == 1 && B <= 16 && (hd == 64 || hd == 128);
   for (int l = 0; l < L; ++l) {
+    hdf::QkvEpiArgs fused_ctx{}, fused_blk{};
     // Q, K_b, V_b with RoPE at T_s + k (and the context rows' K/V when grouped).
     if (shared) {
       const char* wkv = static_cast<const char*>(w->w_qkv[l]) + size_t(d) * d * el;
@@ -663,7 +667,12 @@ static hdf_status draft_block_impl(const hdf_drafter* w, int n_seq, int B, const
       be.pq = parts_q; be.ld_q = d; be.zs_q = int64_t(M) * d;
       be.pkv = parts_kv + size_t(n_new) * 2 * d; be.ld_kv = 2 * int64_t(d);
       be.zs_kv = ce.zs_kv;
-      HDF_TRY(hdf::launch_qkv_epilogue2(bf, ce, be, s));
+      if (fuse_epi) {
+        fused_ctx = ce;
+        fused_blk = be;
+      } else {
+        HDF_TRY(hdf::launch_qkv_epilogue2(bf, ce, be, s));
+      }
     } else if (grouped) {
       const char* wkv = static_cast<const char*>(w->w_qkv[l]) + size_t(d) * d * el;
       const int rows = int(n_new);
@@ -690,6 +699,10 @@ static hdf_status draft_block_impl(const hdf_drafter* w, int n_seq, int B, const
     aa.n_chunks = n_chunks; aa.chunk_len = P.chunk_len;
     aa.scale_log2 = float(1.4426950408889634 / sqrt(double(hd)));
     aa.part_o = part_o; aa.part_ml = part_ml;
+    aa.fuse_epi = fuse_epi ? 1 : 0;
+    aa.new_offsets = new_offsets;
+    aa.epi_ctx = fused_ctx;
+    aa.epi_blk = fused_blk;
     HDF_TRY(hdf::launch_attention(bf, aa, attn, s));
 
     // h += O Wo^T; u = RMSNorm(h) * mlp_norm.

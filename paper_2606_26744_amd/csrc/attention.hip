@@ -28,8 +28,15 @@
 // LDS and issues no dependent global loads (the chunk's cache tiles are looked up
 // once, into LDS, before it); the two waves of a SIMD overlap one's loads with the
 // other's products.  The waves of a workgroup merge through LDS at the end.
+//
+// When one workgroup owns a (sequence, head) and the projections left split-K partials,
+// the workgroup first runs the projection epilogue of its head (qkv_epi.hpp): the
+// sequence's new context rows into the cache, its block rows' Q into the Q buffer and K,
+// V into the block buffers, all read back only by this workgroup; that saves the
+// epilogue's own launch.
 #include "common.hpp"
 #include "kernels.hpp"
+#include "qkv_epi.hpp"
 
 namespace hdf {
 
@@ -48,7 +55,9 @@ constexpr int kAttnWaves = 8;
 constexpr int kAttnThreads = 64 * kAttnWaves;
 
 // Two waves per SIMD (one workgroup per CU): 256 VGPRs per wave at most.
-template <int HD>
+// FUSE: the workgroup first runs the projection epilogue of its (sequence, head) (AttnArgs
+// fuse_epi; only with one workgroup per (sequence, head)).
+template <int HD, bool FUSE>
 __global__ void __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)))
 attn_bf16_kernel(AttnArgs a, bf16_t* __restrict__ out) {
   constexpr int NJ = HD / 32;   // MFMA steps over the head dimension for S
@@ -71,6 +80,36 @@ attn_bf16_kernel(AttnArgs a, bf16_t* __restrict__ out) {
   const bool direct = a.n_chunks == 1;
   const bool blk_chunk = chunk == a.n_chunks;   // the block's own workgroup
   if (!direct && !blk_chunk && chunk >= attn_ctx_chunks(a, T)) return;  // past the context
+
+  if constexpr (FUSE) {
+    // Head h of this sequence's projected rows, 16 rows a round: threads 0-255 its
+    // context rows (new_offsets[s] .. new_offsets[s+1]-1 of epi_ctx), threads 256-511
+    // its B block rows (epi_blk).  The keys and values land in the cache and the block
+    // buffers and Q in the Q buffer, where the code below reads them; nobody else reads
+    // them before the next kernel.  Both halves run every round (the tile function holds
+    // workgroup barriers); an empty tile stores nothing and reads row 0.
+    static_assert(kAttnThreads == 2 * kQkvThreads, "two epilogue tiles per round");
+    __shared__ QkvEpiSmem<HD> esm[2];
+    const int half = threadIdx.x / kQkvThreads, et = threadIdx.x % kQkvThreads;
+    // The sequence's context rows, clamped to the rows the epilogue holds (offsets past
+    // them have no plan entries and no partials; the stand-alone epilogue stops there too).
+    const int c1 = min(max(a.new_offsets[s + 1], 0), a.epi_ctx.M);
+    const int c0 = min(max(a.new_offsets[s], 0), c1);
+    const int rounds = max((c1 - c0 + kQkvRows - 1) / kQkvRows, (a.B + kQkvRows - 1) / kQkvRows);
+    for (int it = 0; it < rounds; ++it) {
+      if (half == 0) {
+        const int r0 = c0 + it * kQkvRows;
+        const int rows = max(0, min(kQkvRows, c1 - r0));
+        qkv_epi_tile<bf16_t, HD>(a.epi_ctx, rows > 0 ? r0 : 0, rows, h, et, esm[0]);
+      } else {
+        const int rows = max(0, min(kQkvRows, a.B - it * kQkvRows));
+        qkv_epi_tile<bf16_t, HD>(a.epi_blk, rows > 0 ? s * a.B + it * kQkvRows : 0, rows, h, et,
+                                 esm[1]);
+      }
+    }
+    __threadfence_block();
+    __syncthreads();
+  }
 
   // Context keys [k_lo, k_hi) of the chunk in 64-row tiles (the sequence's tile t is
   // cache tile kv_offsets[s]/64 + t, or page page_table[s][t] of a paged cache); the
@@ -411,10 +450,19 @@ hipError_t launch_attention(bool bf16, const AttnArgs& a, void* out, hipStream_t
   const int nqg = (a.B + 15) / 16;
   const dim3 grid(a.n_chunks == 1 ? 1 : a.n_chunks + 1, a.nh, a.n_seq * nqg);
   bf16_t* o = static_cast<bf16_t*>(out);
+  if (a.fuse_epi) {
+    // The projection epilogue runs in the attention workgroups: one per (sequence, head).
+    if (a.n_chunks != 1 || nqg != 1 || a.new_offsets == nullptr) return hipErrorInvalidValue;
+    if (a.hd == 128)
+      hipLaunchKernelGGL((attn_bf16_kernel<128, true>), grid, dim3(kAttnThreads), 0, s, a, o);
+    else
+      hipLaunchKernelGGL((attn_bf16_kernel<64, true>), grid, dim3(kAttnThreads), 0, s, a, o);
+    return hipGetLastError();
+  }
   if (a.hd == 128)
-    hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(kAttnThreads), 0, s, a, o);
+    hipLaunchKernelGGL((attn_bf16_kernel<128, false>), grid, dim3(kAttnThreads), 0, s, a, o);
   else
-    hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(kAttnThreads), 0, s, a, o);
+    hipLaunchKernelGGL((attn_bf16_kernel<64, false>), grid, dim3(kAttnThreads), 0, s, a, o);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_chunks == 1) return e;
   const size_t lds = size_t(2) * 16 * (a.n_chunks + 1) * sizeof(float);

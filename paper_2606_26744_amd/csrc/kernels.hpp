@@ -205,6 +205,13 @@ struct AttnArgs {
   float scale_log2;          // log2(e) / sqrt(hd)
   float* part_o;             // [n_seq][nh][n_chunks+1][QB][hd]
   float* part_ml;            // [n_seq][nh][n_chunks+1][QB][2]
+  // Projection epilogue run by the attention kernel itself (bf16, one workgroup per
+  // (sequence, head): n_chunks == 1, B <= 16): the workgroup of (s, h) first finishes head
+  // h of the context rows new_offsets[s] .. new_offsets[s+1]-1 of epi_ctx and of the block
+  // rows of s (epi_blk), then attends.  fuse_epi = 0: the epilogue ran before.
+  int fuse_epi;
+  const int32_t* new_offsets;  // [n_seq+1]
+  QkvEpiArgs epi_ctx, epi_blk;
 };
 
 // Longest context chunk of one bf16 attention workgroup.
