@@ -25,7 +25,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-# HBM bytes of one 128-row hdf_lm_head_argmax call (the GEMM and the finalize kernel) from
+# HBM bytes of one 128-row LM-head GEMM launch (plus the finalize kernel's 3 KiB) from
 # the two rocprofv3 --pmc runs recorded in profiles/lm_head_argmax_hbm_counters.md:
 # FETCH_SIZE x 1.99997 + WRITE_SIZE x 1.000 KiB, the factors a 2 GiB device copy reads on
 # the same counters.  Valid only for the kernel source it was measured on: reported as
@@ -724,7 +724,8 @@ def main():
     cold = None if a.no_cold_cache else cold_cache_step(torch, h, bufs, args, tg, a.steps)
     sweep = None if a.no_m_sweep else lm_head_m_sweep(torch, synth, hdf, h, wl.d)
     acc = out["accept_len"].cpu().numpy()
-    # LM head roofline: algorithmic bytes of one launch (weights + hidden + outputs).
+    # LM head roofline: algorithmic bytes of one hdf_lm_head_argmax_keys call, the LM-head
+    # GEMM (weights + hidden states + the per-row argmax keys it leaves).
     d, V, M = wl.d, wl.drafter.vocab, n_seq * B
     lm_bytes = V * d * 2 + M * d * 2 + M * 8
     lm_us = lm_head_us

@@ -314,6 +314,17 @@ hdf_status hdf_lm_head_argmax(const void* hidden, const void* W_lm, int64_t M, i
                               hdf_dtype dtype, int32_t* argmax, float* max_logit, float* logits,
                               void* ws, size_t ws_bytes, hdf_stream_t stream);
 
+/* The GEMM of hdf_lm_head_argmax alone (Sec. 2.3), for the greedy step that hands its
+ * argmax straight to the acceptance (hdf_accept_keys): every row's (maximum, lowest
+ * column) is folded into the workspace as a packed 64-bit key and left there; nothing is
+ * written to argmax or max_logit and the workspace is not cleared.  The next call on the
+ * same workspace must be hdf_accept_keys over the same rows (M = n_seq * B), which turns
+ * the keys into argmax / max_logit and hands the workspace back zeroed.
+ * hidden, W_lm, M, d, vocab, dtype, ws, ws_bytes and limits: as hdf_lm_head_argmax. */
+hdf_status hdf_lm_head_argmax_keys(const void* hidden, const void* W_lm, int64_t M, int d,
+                                   int vocab, hdf_dtype dtype, void* ws, size_t ws_bytes,
+                                   hdf_stream_t stream);
+
 /* hdf_lm_head_argmax for callers that cannot allocate device memory (code under HIP
  * graph capture, serving loops or harnesses that forbid allocation): the same kernels and
  * results, with no workspace argument.  The per-row argmax keys live in a library-owned
@@ -353,6 +364,20 @@ hdf_status hdf_lm_head_argmax_noalloc(const void* hidden, const void* W_lm, int6
 hdf_status hdf_accept(const int32_t* draft, int draft_stride, const int32_t* target, int n_seq,
                       int K, int32_t* accept_len, int32_t* next_anchor, int32_t* commit_offsets,
                       int32_t* commit_tokens, hdf_stream_t stream);
+
+/* The finalisation of hdf_lm_head_argmax_keys and hdf_accept on the blocks' drafts in one
+ * launch (Sec. 2.3 argmax; Sec. 1 and Sec. 3.4 acceptance).  The workspace holds the
+ * packed keys of the M = n_seq * B block rows (row s*B + k is slot k of sequence s) that
+ * hdf_lm_head_argmax_keys left in it.  Writes argmax [M] int32 and max_logit [M] fp32 (may
+ * be NULL) exactly as hdf_lm_head_argmax would, clears the keys (the workspace is handed
+ * back zeroed), then runs hdf_accept with draft = argmax + 1, draft_stride = B and K = B - 1
+ * (the drafts are slots 1 .. B-1).
+ * ws        the workspace of the hdf_lm_head_argmax_keys call (8-byte aligned)
+ * target, accept_len, next_anchor, commit_offsets, commit_tokens: as hdf_accept
+ * Limits: n_seq >= 0, 1 <= B <= 1025, n_seq * B < 2^31. */
+hdf_status hdf_accept_keys(void* ws, int n_seq, int B, int32_t* argmax, float* max_logit,
+                           const int32_t* target, int32_t* accept_len, int32_t* next_anchor,
+                           int32_t* commit_offsets, int32_t* commit_tokens, hdf_stream_t stream);
 
 /* Context growth after a round (Sec. 1: the n_s accepted drafts and the target's token
  * after them join the context; Sec. 3.4: tau = n_s + 1): for every s,

@@ -1,5 +1,6 @@
 // Greedy acceptance (Sec. 1: the target keeps the longest agreeing draft prefix;
-// Sec. 3.4: tau, the accepted length per round).
+// Sec. 3.4: tau, the accepted length per round), optionally preceded by the LM head's
+// argmax finalisation (hdf_accept_keys).
 //
 // One workgroup of 16 waves, sequences in chunks of 1024:
 //   1. one wave per sequence: its lanes compare 64 draft positions at once (ballot of
@@ -15,16 +16,30 @@ namespace hdf {
 constexpr int kAcceptThreads = 1024;
 constexpr int kAcceptWaves = kAcceptThreads / kWave;
 
+// keys != NULL: the workgroup first turns the LM head's packed argmax keys of rows
+// 0 .. M-1 into argmax (and max_logit) and clears them, then reads its drafts from the
+// argmax it has just written (draft points into it); the workgroup barrier with the fence
+// before it makes those stores visible to every wave.
 __global__ void __launch_bounds__(kAcceptThreads)
-accept_kernel(const int32_t* __restrict__ draft, int stride, const int32_t* __restrict__ target,
+accept_kernel(const int32_t* draft, int stride, const int32_t* __restrict__ target,
               int n_seq, int K, int32_t* __restrict__ acc, int32_t* __restrict__ anchor,
-              int32_t* __restrict__ offs, int32_t* __restrict__ toks) {
+              int32_t* __restrict__ offs, int32_t* __restrict__ toks,
+              unsigned long long* __restrict__ keys, int64_t M, int32_t* argmax,
+              float* __restrict__ max_logit) {
   __shared__ int len[kAcceptThreads];     // n_s + 1, then the exclusive offsets
   __shared__ int nacc[kAcceptThreads];    // n_s
   __shared__ int wsum[kAcceptWaves];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wid = tid >> 6;
+  if (keys != nullptr) {
+    for (int64_t i = tid; i < M; i += kAcceptThreads) {
+      decode_argmax_key(keys[i], argmax + i, max_logit != nullptr ? max_logit + i : nullptr);
+      keys[i] = 0ull;   // the workspace is handed back zeroed
+    }
+    __threadfence_block();
+    __syncthreads();
+  }
   int carry = 0;
   for (int base = 0; base < n_seq; base += kAcceptThreads) {
     const int cnt = min(kAcceptThreads, n_seq - base);
@@ -95,7 +110,17 @@ hipError_t launch_accept(const int32_t* draft, int stride, const int32_t* target
                          int K, int32_t* acc, int32_t* anchor, int32_t* offs, int32_t* toks,
                          hipStream_t s) {
   hipLaunchKernelGGL(accept_kernel, dim3(1), dim3(kAcceptThreads), 0, s, draft, stride, target,
-                     n_seq, K, acc, anchor, offs, toks);
+                     n_seq, K, acc, anchor, offs, toks, nullptr, int64_t(0), nullptr, nullptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_accept_keys(unsigned long long* keys, int64_t M, int32_t* argmax,
+                              float* max_logit, int draft_off, int stride,
+                              const int32_t* target, int n_seq, int K, int32_t* acc,
+                              int32_t* anchor, int32_t* offs, int32_t* toks, hipStream_t s) {
+  hipLaunchKernelGGL(accept_kernel, dim3(1), dim3(kAcceptThreads), 0, s, argmax + draft_off,
+                     stride, target, n_seq, K, acc, anchor, offs, toks, keys, M, argmax,
+                     max_logit);
   return hipGetLastError();
 }
 

@@ -815,6 +815,52 @@ hdf_status hdf_lm_head_argmax(const void* hidden, const void* W_lm, int64_t M, i
   return ok();
 }
 
+hdf_status hdf_lm_head_argmax_keys(const void* hidden, const void* W_lm, int64_t M, int d,
+                                   int vocab, hdf_dtype dtype, void* ws, size_t ws_bytes,
+                                   hdf_stream_t stream) {
+  if (dtype != HDF_F32 && dtype != HDF_BF16) return fail(HDF_E_INVALID, "lm_head_keys: bad dtype");
+  if (M < 0) return fail(HDF_E_INVALID, "lm_head_keys: M < 0");
+  if (d <= 0 || d % 64 != 0)
+    return fail(HDF_E_INVALID, "lm_head_keys: d=%d not a positive multiple of 64", d);
+  if (vocab < 1) return fail(HDF_E_INVALID, "lm_head_keys: vocab < 1");
+  if (M == 0) return ok();
+  if (hidden == nullptr || W_lm == nullptr) return fail(HDF_E_INVALID, "lm_head_keys: null pointer");
+  if (!aligned16(hidden) || !aligned16(W_lm))
+    return fail(HDF_E_INVALID, "lm_head_keys: hidden and W_lm must be 16-byte aligned");
+  const size_t need = hdf_lm_head_workspace(M, vocab);
+  if (ws == nullptr || ws_bytes < need)
+    return fail(HDF_E_WORKSPACE, "lm_head_keys: workspace of %zu bytes needed, %zu given", need,
+                ws_bytes);
+  if ((reinterpret_cast<uintptr_t>(ws) & 7u) != 0)
+    return fail(HDF_E_INVALID, "lm_head_keys: workspace must be 8-byte aligned");
+  hipError_t e = hdf::launch_lm_head_keys(dtype == HDF_BF16, hidden, W_lm, M, d, vocab,
+                                          static_cast<unsigned long long*>(ws), nullptr,
+                                          reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "lm_head_keys launch");
+  return ok();
+}
+
+hdf_status hdf_accept_keys(void* ws, int n_seq, int B, int32_t* argmax, float* max_logit,
+                           const int32_t* target, int32_t* accept_len, int32_t* next_anchor,
+                           int32_t* commit_offsets, int32_t* commit_tokens, hdf_stream_t stream) {
+  if (n_seq < 0) return fail(HDF_E_INVALID, "accept_keys: n_seq < 0");
+  if (B < 1 || B > 1025) return fail(HDF_E_INVALID, "accept_keys: B=%d outside [1, 1025]", B);
+  if (n_seq == 0) return ok();
+  if (ws == nullptr || argmax == nullptr || target == nullptr || accept_len == nullptr ||
+      next_anchor == nullptr)
+    return fail(HDF_E_INVALID, "accept_keys: null pointer");
+  if ((reinterpret_cast<uintptr_t>(ws) & 7u) != 0)
+    return fail(HDF_E_INVALID, "accept_keys: workspace must be 8-byte aligned");
+  const int64_t M = int64_t(n_seq) * B;
+  if (M > INT32_MAX) return fail(HDF_E_UNSUPPORTED, "accept_keys: n_seq*B exceeds int32 offsets");
+  hipError_t e = hdf::launch_accept_keys(static_cast<unsigned long long*>(ws), M, argmax,
+                                         max_logit, 1, B, target, n_seq, B - 1, accept_len,
+                                         next_anchor, commit_offsets, commit_tokens,
+                                         reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "accept_keys launch");
+  return ok();
+}
+
 // ---------------------------------------------------------- LM head without a workspace
 // For callers that cannot allocate: the per-row argmax keys live in this file-scope device
 // array (one copy per GPU, held until the process ends) instead of a workspace.  In host

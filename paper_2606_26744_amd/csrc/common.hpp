@@ -118,4 +118,12 @@ __device__ __forceinline__ float f32_from_order_key(uint32_t k) {
   return __uint_as_float(u);
 }
 
+// A row's packed argmax key (order key of the maximum << 32 | ~column): its column and,
+// when max_logit is given, the maximum.
+__device__ __forceinline__ void decode_argmax_key(unsigned long long k, int32_t* argmax,
+                                                  float* max_logit) {
+  *argmax = int32_t(0xFFFFFFFFu - uint32_t(k & 0xFFFFFFFFull));
+  if (max_logit != nullptr) *max_logit = f32_from_order_key(uint32_t(k >> 32));
+}
+
 }  // namespace hdf

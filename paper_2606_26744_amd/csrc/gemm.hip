@@ -627,9 +627,7 @@ __global__ void argmax_finalize_kernel(unsigned long long* keys, int64_t M, int3
                                        float* max_logit) {
   const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i >= M) return;
-  const unsigned long long k = keys[i];
-  argmax[i] = int32_t(0xFFFFFFFFu - uint32_t(k & 0xFFFFFFFFull));
-  if (max_logit != nullptr) max_logit[i] = f32_from_order_key(uint32_t(k >> 32));
+  decode_argmax_key(keys[i], argmax + i, max_logit != nullptr ? max_logit + i : nullptr);
   keys[i] = 0ull;   // the workspace is handed back zeroed
 }
 
@@ -880,14 +878,10 @@ GemmPlan lm_head_plan(int64_t) {
   return GemmPlan{8, 1, 2};
 }
 
-hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t M, int d, int V,
-                          unsigned long long* keys, int32_t* argmax, float* max_logit,
-                          float* logits, hipStream_t s) {
-  // keys are zero on entry (the workspace contract): the finalize pass clears them.
-  const int threads = 256;
-  const unsigned blocks = unsigned((M + threads - 1) / threads);
-  hipError_t e;
-  // Rows are processed in chunks that keep the int32 tile arithmetic in range.
+hipError_t launch_lm_head_keys(bool bf16, const void* hidden, const void* W, int64_t M, int d,
+                               int V, unsigned long long* keys, float* logits, hipStream_t s) {
+  // keys are zero on entry (the workspace contract); the GEMM folds every row's maximum
+  // into them.  Rows are processed in chunks that keep the int32 tile arithmetic in range.
   const int64_t chunk = 1 << 20;
   for (int64_t r0 = 0; r0 < M; r0 += chunk) {
     const int rows = int(M - r0 < chunk ? M - r0 : chunk);
@@ -898,9 +892,20 @@ hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t 
     a.M = rows; a.N = V; a.K = d;
     a.C = logits != nullptr ? logits + r0 * V : nullptr;
     a.keys = keys + r0;
-    e = launch_gemm_any(bf16, kEpiArgmax, a, lm_head_plan(M), s);
+    const hipError_t e = launch_gemm_any(bf16, kEpiArgmax, a, lm_head_plan(M), s);
     if (e != hipSuccess) return e;
   }
+  return hipSuccess;
+}
+
+hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t M, int d, int V,
+                          unsigned long long* keys, int32_t* argmax, float* max_logit,
+                          float* logits, hipStream_t s) {
+  const hipError_t e = launch_lm_head_keys(bf16, hidden, W, M, d, V, keys, logits, s);
+  if (e != hipSuccess) return e;
+  // The finalize pass turns the keys into outputs and clears them.
+  const int threads = 256;
+  const unsigned blocks = unsigned((M + threads - 1) / threads);
   hipLaunchKernelGGL(argmax_finalize_kernel, dim3(blocks), dim3(threads), 0, s, keys, M, argmax,
                      max_logit);
   return hipGetLastError();

@@ -23,6 +23,13 @@ hipError_t launch_hc_reduce(bool bf16, int m, const void* H, const void* Wg, con
 hipError_t launch_accept(const int32_t* draft, int stride, const int32_t* target, int n_seq,
                          int K, int32_t* acc, int32_t* anchor, int32_t* offs, int32_t* toks,
                          hipStream_t s);
+// The LM head's argmax finalisation and the acceptance in one workgroup: rows 0 .. M-1 of
+// keys -> argmax (and max_logit, may be NULL), keys cleared; then launch_accept's work
+// with draft = argmax + draft_off.
+hipError_t launch_accept_keys(unsigned long long* keys, int64_t M, int32_t* argmax,
+                              float* max_logit, int draft_off, int stride,
+                              const int32_t* target, int n_seq, int K, int32_t* acc,
+                              int32_t* anchor, int32_t* offs, int32_t* toks, hipStream_t s);
 
 // ---------------------------------------------------------------- GEMM (gemm.hip)
 constexpr int kEpiPartial = 0;  // fp32 C / split-K partials
@@ -88,6 +95,9 @@ hipError_t launch_gemm_kv(const void* A, int64_t lda, const void* B, int M, int 
 hipError_t launch_lm_head(bool bf16, const void* hidden, const void* W, int64_t M, int d, int V,
                           unsigned long long* keys, int32_t* argmax, float* max_logit,
                           float* logits, hipStream_t s);
+// The GEMM of launch_lm_head only: the keys are left folded, not finalised or cleared.
+hipError_t launch_lm_head_keys(bool bf16, const void* hidden, const void* W, int64_t M, int d,
+                               int V, unsigned long long* keys, float* logits, hipStream_t s);
 // Tile shape of the LM head's bf16 kernel for M rows (waves, blocks per wave).
 GemmPlan lm_head_plan(int64_t M);
 

@@ -29,7 +29,7 @@ EXPORTS = ("hdf_last_error", "hdf_version", "hdf_hc_reduce", "hdf_rope_table",
            "hdf_sample_workspace", "hdf_sample_tokens", "hdf_accept_sample_workspace",
            "hdf_accept_sample", "hdf_kl_forward_workspace", "hdf_kl_forward",
            "hdf_advance_context", "hdf_kv_write_rows", "hdf_kv_read_rows",
-           "hdf_lm_head_argmax_noalloc")
+           "hdf_lm_head_argmax_noalloc", "hdf_lm_head_argmax_keys", "hdf_accept_keys")
 
 
 class HdfError(RuntimeError):
@@ -111,6 +111,10 @@ def lib() -> ctypes.CDLL:
     L.hdf_lm_head_argmax_noalloc.argtypes = [_P, _P, _I64, _I, _I, _I, _P, _P, _P, _P]
     L.hdf_accept.restype = _I
     L.hdf_accept.argtypes = [_P, _I, _P, _I, _I, _P, _P, _P, _P, _P]
+    L.hdf_lm_head_argmax_keys.restype = _I
+    L.hdf_lm_head_argmax_keys.argtypes = [_P, _P, _I64, _I, _I, _I, _P, _SZ, _P]
+    L.hdf_accept_keys.restype = _I
+    L.hdf_accept_keys.argtypes = [_P, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P]
     _U64 = ctypes.c_uint64
     L.hdf_sample_workspace.restype = _SZ
     L.hdf_sample_workspace.argtypes = [_I64, _I]
@@ -379,6 +383,50 @@ def lm_head_argmax(hidden: torch.Tensor, w_lm: PackedWeight, *, want_logits: boo
     _check(lib().hdf_lm_head_argmax(_ptr(hidden), _ptr(w_lm), M, d, V, _dt(hidden), _ptr(am),
                                     _ptr(mx), _ptr(lg), _ptr(ws), ws.numel(), _stream(stream)))
     return am, mx, lg
+
+
+def lm_head_argmax_keys(hidden: torch.Tensor, w_lm: PackedWeight, ws: torch.Tensor,
+                        stream=None):
+    """hdf_lm_head_argmax_keys: the LM-head GEMM alone; the packed argmax keys of the M
+    rows stay in `ws` (a zeroed workspace of lm_head_workspace(M, V) bytes) for
+    accept_keys."""
+    if not isinstance(w_lm, PackedWeight):
+        raise TypeError("w_lm must be packed with pack_weight()")
+    M, d = hidden.shape
+    V = w_lm.N
+    if w_lm.K != d or w_lm.dtype != hidden.dtype:
+        raise ValueError("hidden and w_lm disagree in width or dtype")
+    if ws is None or ws.numel() < lm_head_workspace(M, V):
+        raise ValueError("lm_head_argmax_keys needs a workspace of lm_head_workspace(M, V) bytes")
+    _dev(hidden, w_lm.data, ws)
+    _check(lib().hdf_lm_head_argmax_keys(_ptr(hidden), _ptr(w_lm), M, d, V, _dt(hidden),
+                                         _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def accept_keys(ws: torch.Tensor, target: torch.Tensor, B: int, *, argmax: torch.Tensor,
+                max_logit: Optional[torch.Tensor] = None, commits: bool = True, out=None,
+                stream=None):
+    """hdf_accept_keys: argmax (and max_logit) of the n_seq*B block rows from the keys in
+    `ws`, the keys cleared, then the acceptance of the drafts (slots 1..B-1) against
+    target [n_seq, B] int32.  Returns (accept_len, next_anchor, commit_offsets,
+    commit_tokens); out: optional preallocated tuple of those."""
+    n_seq = target.shape[0]
+    if target.shape[1] != B:
+        raise ValueError("target must be [n_seq, B] (K + 1 = B tokens per sequence)")
+    if argmax.numel() < n_seq * B:
+        raise ValueError("argmax must hold n_seq * B rows")
+    dev = target.device
+    if out is not None:
+        acc, anc, offs, toks = out
+    else:
+        acc = torch.empty(n_seq, dtype=torch.int32, device=dev)
+        anc = torch.empty(n_seq, dtype=torch.int32, device=dev)
+        offs = torch.empty(n_seq + 1, dtype=torch.int32, device=dev) if commits else None
+        toks = torch.empty(max(1, n_seq * B), dtype=torch.int32, device=dev) if commits else None
+    _dev(ws, target, argmax, max_logit, acc, anc, offs, toks)
+    _check(lib().hdf_accept_keys(_ptr(ws), n_seq, B, _ptr(argmax), _ptr(max_logit), _ptr(target),
+                                 _ptr(acc), _ptr(anc), _ptr(offs), _ptr(toks), _stream(stream)))
+    return acc, anc, offs, toks
 
 
 # ----------------------------------------------------------------------------- drafter

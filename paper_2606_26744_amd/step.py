@@ -6,6 +6,9 @@ libhdf's kernels:
     hdf_draft_block      Y -> KV cache rows; block [anchor, mask...] -> hidden
     hdf_lm_head_argmax   hidden -> argmax per slot
     hdf_accept           drafts (slots 1..B-1) vs the target's tokens
+With targets and no logits asked for, the last two are hdf_lm_head_argmax_keys (the
+LM-head GEMM) and hdf_accept_keys (the argmax finalisation and the acceptance in one
+launch), with the same outputs.
 This module only allocates device buffers (once) and passes pointers.
 """
 from __future__ import annotations
@@ -74,6 +77,16 @@ def drafter_step(handle: hdf.DrafterHandle, bufs: StepBuffers, *, H_new: torch.T
                        kv_offsets=kv_offsets, kv_k=kv_k, kv_vt=kv_vt, tokens=tokens,
                        hidden=bufs.hidden, ws=bufs.ws, stream=stream)
     mark(2)
+    if targets is not None and not logits:
+        n_seq, B = tokens.shape
+        hdf.lm_head_argmax_keys(bufs.hidden, handle.w_lm, bufs.lm_ws, stream=stream)
+        mark(3)
+        acc, anc, offs, toks = hdf.accept_keys(bufs.lm_ws, targets, B, argmax=bufs.argmax,
+                                               max_logit=bufs.max_logit, stream=stream)
+        mark(4)
+        return {"Y": bufs.Y, "hidden": bufs.hidden, "argmax": bufs.argmax,
+                "max_logit": bufs.max_logit, "logits": None, "accept_len": acc,
+                "next_anchor": anc, "commit_offsets": offs, "commit_tokens": toks}
     am, mx, lg = hdf.lm_head_argmax(bufs.hidden, handle.w_lm, want_logits=logits,
                                     ws=bufs.lm_ws, out=(bufs.argmax, bufs.max_logit),
                                     stream=stream)

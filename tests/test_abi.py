@@ -71,6 +71,27 @@ def test_accept_validation():
     assert _status(L.hdf_accept(None, 15, None, 0, 15, None, None, None, None, None)) == "HDF_OK"
 
 
+def test_keys_path_validation():
+    L = hdf.lib()
+    fake = ctypes.c_void_p(4096)
+    odd = ctypes.c_void_p(4100)
+    # hdf_lm_head_argmax_keys: width, vocabulary, pointers, workspace size and alignment
+    assert _status(L.hdf_lm_head_argmax_keys(fake, fake, 16, 100, 1000, 1, fake, 1 << 20, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_lm_head_argmax_keys(fake, fake, 16, 128, 0, 1, fake, 1 << 20, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_lm_head_argmax_keys(None, fake, 16, 128, 1000, 1, fake, 1 << 20, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_lm_head_argmax_keys(fake, fake, 16, 128, 1000, 1, fake, 8, None)) == "HDF_E_WORKSPACE"
+    assert _status(L.hdf_lm_head_argmax_keys(fake, fake, 16, 128, 1000, 1, odd, 1 << 20, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_lm_head_argmax_keys(None, None, 0, 128, 1000, 1, None, 0, None)) == "HDF_OK"
+    # hdf_accept_keys: sizes, pointers, workspace alignment
+    assert _status(L.hdf_accept_keys(fake, -1, 16, fake, None, fake, fake, fake, None, None, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_accept_keys(fake, 2, 0, fake, None, fake, fake, fake, None, None, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_accept_keys(fake, 2, 1026, fake, None, fake, fake, fake, None, None, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_accept_keys(fake, 2, 16, None, None, fake, fake, fake, None, None, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_accept_keys(odd, 2, 16, fake, None, fake, fake, fake, None, None, None)) == "HDF_E_INVALID"
+    assert _status(L.hdf_accept_keys(fake, 1 << 30, 16, fake, None, fake, fake, fake, None, None, None)) == "HDF_E_UNSUPPORTED"
+    assert _status(L.hdf_accept_keys(None, 0, 16, None, None, None, None, None, None, None, None)) == "HDF_OK"
+
+
 def test_rope_table_host_values():
     import math
     t = hdf.rope_table(5, 8, 10000.0)
