@@ -25,13 +25,13 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-# HBM bytes of one 128-row LM-head GEMM launch (plus the finalize kernel's 3 KiB) from
-# the two rocprofv3 --pmc runs recorded in profiles/lm_head_argmax_hbm_counters.md:
+# HBM bytes of one 128-row LM-head GEMM launch (hdf_lm_head_argmax_keys) from the two
+# rocprofv3 --pmc runs recorded in profiles/lm_head_argmax_hbm_counters.md:
 # FETCH_SIZE x 1.99997 + WRITE_SIZE x 1.000 KiB, the factors a 2 GiB device copy reads on
 # the same counters.  Valid only for the kernel source it was measured on: reported as
 # null once the code of gemm.hip or common.hpp changes.
-LM_HEAD_TRAFFIC = {"source_sha": "436f80cdaf898b2f",
-                   "bytes": ((532934.0 + 1.3) * 1.99997 + (253.0 + 2.0) * 1.000) * 1024}
+LM_HEAD_TRAFFIC = {"source_sha": "22c0fa4038ecf59e",
+                   "bytes": (532957.9 * 1.99997 + 253.0 * 1.000) * 1024}
 BF16_PEAK_TFLOPS = 2500.0
 METRIC = "draft blocks/sec at d=4096,B=16,V=129280; reducer HBM GB/s; MFMA util %"
 
