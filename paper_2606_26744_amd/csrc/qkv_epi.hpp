@@ -11,8 +11,11 @@
 // Rows r0 .. r0 + rows - 1 of the argument set; rows may be 0 (the call then stores
 // nothing), in which case row r0 must still be a row of the partial buffers, since the
 // loads are issued unpredicated.  kQkvThreads threads take part (tid 0 .. kQkvThreads - 1);
-// the function holds two workgroup barriers, which every thread of the workgroup must
-// reach the same number of times.
+// the function holds three workgroup barriers, which every thread of the workgroup must
+// reach the same number of times.  The first one lets back-to-back calls on the same
+// `sm` follow each other: the row table of a call is written only after every thread has
+// finished reading the previous call's.  The barriers order LDS traffic only: the
+// global stores of a call may still be in flight when it returns.
 #pragma once
 
 #include "common.hpp"
@@ -81,6 +84,7 @@ __device__ __forceinline__ void qkv_epi_tile(const QkvEpiArgs& a, int r0, int ro
   static_assert(kQkvRows * 2 * OCT <= kQkvThreads && kQkvRows * VOCT <= kQkvThreads &&
                     (kQkvRows / 8) * HD <= kQkvThreads,
                 "one item of each kind per thread");
+  lds_barrier();
   if (tid < rows) {
     int pos, s, k;
     int64_t drow;
@@ -90,7 +94,7 @@ __device__ __forceinline__ void qkv_epi_tile(const QkvEpiArgs& a, int r0, int ro
     sm.slot[tid] = k;
     sm.drow[tid] = drow;
   }
-  __syncthreads();
+  lds_barrier();
   const int nrot = 2 - a.first_part;  // Q and K, or K only
 
   // This thread's rotated item (row rr, part, octet o: dims i0..i0+7 and i0+HALF..) and
@@ -172,7 +176,7 @@ __device__ __forceinline__ void qkv_epi_tile(const QkvEpiArgs& a, int r0, int ro
     t[0] = xv[0].x; t[1] = xv[0].y; t[2] = xv[0].z; t[3] = xv[0].w;
     t[4] = xv[1].x; t[5] = xv[1].y; t[6] = xv[1].z; t[7] = xv[1].w;
   }
-  __syncthreads();
+  lds_barrier();
   // V out: item (dim i, group of eight rows).  Eight new rows at eight consecutive cache
   // rows starting at a multiple of 8 are one contiguous run of the value tile layout.
   const int i = tid % HD, g = tid / HD;

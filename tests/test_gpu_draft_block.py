@@ -104,6 +104,20 @@ def test_many_sequences_attention_chunks_head_dim_128():
              seqs=[2, 30])
 
 
+def test_fused_epilogue_several_rounds():
+    """Warm steps with up to 128 projected rows and B <= 16, so the projection epilogue runs
+    inside the attention kernel, in several 16-row rounds for the longer sequences (70, 33
+    and 17 new rows): every new cache row and the block states against the oracle, at head
+    dims 64 and 128, contiguous and paged."""
+    wl = synth.small_bf16()
+    _compare(DraftCase(wl, [300, 90, 45], [70, 33, 17], sub=21))
+    _compare(DraftCase(wl, [300, 90, 45], [70, 33, 17], sub=22, paged=True, spare_pages=3))
+    wl.drafter = synth.DrafterShape(d=512, n_layers=1, n_heads=4, head_dim=128, d_ff=1024,
+                                    vocab=1000)
+    wl.d = 512
+    _compare(DraftCase(wl, [200, 129, 40], [80, 29, 19], sub=23))
+
+
 def test_no_rope_fp32_multilayer():
     wl = synth.tiny_fp32()
     wl.drafter = synth.DrafterShape(d=256, n_layers=3, n_heads=4, head_dim=64, d_ff=512,
