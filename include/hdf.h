@@ -268,8 +268,10 @@ hdf_status hdf_draft_block(const hdf_drafter* w, int n_seq, int B, const int32_t
  * n_s + 1 accepted positions of every round, Sec. 1).
  * page_table  [n_seq][max_pages] int32 (device): pages 0 .. ceil(T_s/64)-1 of every
  *             sequence must be valid page indices in [0, kv_pages) and no page may be
- *             listed twice among the pages written by this call (new rows); entries
- *             past a sequence's last page are not read.  Not checked on the device.
+ *             listed twice among the pages written by this call (new rows), nor be a
+ *             page of another sequence (pages shared between sequences, such as a common
+ *             prefix, are read-only); entries past a sequence's last page are not read.
+ *             Not checked on the device.
  * max_pages   host: row stride of page_table; max_pages * 64 >= max_ctx
  * kv_pages    host: pages in the pool (kv_pages * 64 < 2^31)
  * new_counts  [n_seq] int32 (device) or NULL.  NULL: every row new_offsets[s] ..
