@@ -192,12 +192,16 @@ gemm_bf16_kernel(GemmArgs p) {
     auto a_store = [&](const u32x4& v, int u) {
       *reinterpret_cast<u32x4*>(&Au[u % NBUF][tid >> 2][(tid & 3) * 8]) = v;
     };
+    // Units past the end are never used: their loads read the activations' first 16
+    // bytes (in L2) instead of the weights again (see load_b below).
     auto b_load = [&](int u, u32x4* dst) {
-      const int64_t kb = (ku0 + min(u, nu - 1)) * (UK / 16);
+      const bool live = u < nu;
+      const int64_t kb = (ku0 + (live ? u : 0)) * (UK / 16);
 #pragma unroll
       for (int ss = 0; ss < 2; ++ss)
 #pragma unroll
-        for (int tn = 0; tn < TN; ++tn) dst[ss * TN + tn] = ld16(Bw[tn] + (kb + ss) * 4 * 512);
+        for (int tn = 0; tn < TN; ++tn)
+          dst[ss * TN + tn] = ld16(live ? Bw[tn] + (kb + ss) * 4 * 512 : A);
     };
     const int arow = lane & 31;
     const int kof = 8 * (lane >> 5);
@@ -263,13 +267,19 @@ gemm_bf16_kernel(GemmArgs p) {
         dst[i] = ld16(A + int64_t(row) * p.lda + k + (c & 7) * 8);
       }
     };
+    // The ring issues STAGES steps past the last one; those are never used.  Their loads
+    // read the activations' first 16 bytes (one line, in L2) rather than the last weight
+    // step again: a re-read of the weights would come from HBM (the non-temporal streams
+    // do not keep them in L2), STAGES of the nk steps extra (O/down: 2 of 8).  The loads
+    // are still issued, so the compiler's outstanding-load counting stays exact.
     auto load_b = [&](int kt, u32x4* dst) {
-      const int64_t kb = int64_t(kt_begin + min(kt, nk - 1)) * (kBK / 16);
+      const bool live = kt < nk;
+      const int64_t kb = int64_t(kt_begin + (live ? kt : 0)) * (kBK / 16);
 #pragma unroll
       for (int q = 0; q < 4; ++q)
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) {
-          const bf16_t* src = Bw[tn] + (kb + q) * 4 * 512;
+          const bf16_t* src = live ? Bw[tn] + (kb + q) * 4 * 512 : A;
           dst[q * TN + tn] = NT ? ld_nt16(src) : ld16(src);
         }
     };
