@@ -165,6 +165,14 @@ def _dev(*ts):
                 raise ValueError("libhdf takes contiguous tensors")
 
 
+def _typed(t: Optional[torch.Tensor], dtype, numel: int, what: str):
+    """The C ABI takes bare pointers, so a tensor of another dtype or too few elements
+    would be read or written past its meaning; checked here instead."""
+    if t is not None and (t.dtype != dtype or t.numel() < numel):
+        raise ValueError(f"{what} must be a {dtype} tensor of at least {numel} elements "
+                         f"(got {t.dtype}, {t.numel()})")
+
+
 # ----------------------------------------------------------------------------- reducer
 
 def hc_reduce(H: torch.Tensor, W_g: torch.Tensor, b_g: torch.Tensor, *, eps: float = 1e-6,
@@ -177,6 +185,10 @@ def hc_reduce(H: torch.Tensor, W_g: torch.Tensor, b_g: torch.Tensor, *, eps: flo
         Y = torch.empty((n, d), dtype=H.dtype, device=H.device)
     if alpha is None and want_alpha:
         alpha = torch.empty((n, m), dtype=torch.float32, device=H.device)
+    _typed(W_g, H.dtype, m * m * d, "W_g")
+    _typed(b_g, torch.float32, m, "b_g")
+    _typed(Y, H.dtype, n * d, "Y")
+    _typed(alpha, torch.float32, n * m, "alpha")
     _dev(H, W_g, b_g, Y, alpha)
     p = ReduceParams(eps, gate_scale, gate_offset, int(per_path_norm))
     _check(lib().hdf_hc_reduce(_ptr(H), _ptr(W_g), _ptr(b_g), n, m, d, _dt(H), ctypes.byref(p),
@@ -222,6 +234,12 @@ def accept(draft: torch.Tensor, target: torch.Tensor, *, K: Optional[int] = None
         offs = torch.empty(n_seq + 1, dtype=torch.int32, device=dev) if commits else None
         toks = (torch.empty(max(1, n_seq * (K + 1)), dtype=torch.int32, device=dev)
                 if commits else None)
+    _typed(target, torch.int32, n_seq * (K + 1), "target")
+    if draft.dtype != torch.int32:
+        raise ValueError("draft must be int32")
+    for t, k, what in ((acc, n_seq, "accept_len"), (anc, n_seq, "next_anchor"),
+                       (offs, n_seq + 1, "commit_offsets"), (toks, n_seq * (K + 1), "commit_tokens")):
+        _typed(t, torch.int32, k, what)
     _dev(target, acc, anc, offs, toks)
     if not draft.is_cuda:
         raise ValueError("libhdf takes device tensors")
@@ -370,6 +388,8 @@ def lm_head_argmax(hidden: torch.Tensor, w_lm: PackedWeight, *, want_logits: boo
         mx = torch.empty(M, dtype=torch.float32, device=dev) if want_max else None
     else:
         am, mx = out
+    _typed(am, torch.int32, M, "argmax")
+    _typed(mx, torch.float32, M, "max_logit")
     if logits_out is not None:
         if logits_out.shape != (M, V) or logits_out.dtype != torch.float32:
             raise ValueError("logits_out must be a [M, V] fp32 tensor")
@@ -413,8 +433,10 @@ def accept_keys(ws: torch.Tensor, target: torch.Tensor, B: int, *, argmax: torch
     n_seq = target.shape[0]
     if target.shape[1] != B:
         raise ValueError("target must be [n_seq, B] (K + 1 = B tokens per sequence)")
-    if argmax.numel() < n_seq * B:
-        raise ValueError("argmax must hold n_seq * B rows")
+    M = n_seq * B
+    _typed(argmax, torch.int32, M, "argmax")
+    _typed(max_logit, torch.float32, M, "max_logit")
+    _typed(target, torch.int32, M, "target")
     dev = target.device
     if out is not None:
         acc, anc, offs, toks = out
@@ -423,6 +445,9 @@ def accept_keys(ws: torch.Tensor, target: torch.Tensor, B: int, *, argmax: torch
         anc = torch.empty(n_seq, dtype=torch.int32, device=dev)
         offs = torch.empty(n_seq + 1, dtype=torch.int32, device=dev) if commits else None
         toks = torch.empty(max(1, n_seq * B), dtype=torch.int32, device=dev) if commits else None
+    for t, k, what in ((acc, n_seq, "accept_len"), (anc, n_seq, "next_anchor"),
+                       (offs, n_seq + 1, "commit_offsets"), (toks, M, "commit_tokens")):
+        _typed(t, torch.int32, k, what)
     _dev(ws, target, argmax, max_logit, acc, anc, offs, toks)
     _check(lib().hdf_accept_keys(_ptr(ws), n_seq, B, _ptr(argmax), _ptr(max_logit), _ptr(target),
                                  _ptr(acc), _ptr(anc), _ptr(offs), _ptr(toks), _stream(stream)))

@@ -213,3 +213,32 @@ def test_fc_reduce_validation():
     # too small a workspace
     st = L.hdf_fc_reduce(fake, fake, None, 10, 4, 256, 1, fake, fake, 16, None)
     assert _status(st) == "HDF_E_WORKSPACE"
+
+
+def test_binding_rejects_wrong_dtypes_and_sizes():
+    """The C ABI takes bare pointers, so the binding checks the dtype and size of the index
+    and output tensors before any call (here with host tensors: the check comes first)."""
+    import torch
+    i32 = torch.zeros(64, dtype=torch.int32)
+    with pytest.raises(ValueError, match="argmax"):
+        hdf.accept_keys(torch.zeros(64 * 8, dtype=torch.uint8), i32.view(4, 16), 16,
+                        argmax=torch.zeros(64, dtype=torch.int64))
+    with pytest.raises(ValueError, match="max_logit"):
+        hdf.accept_keys(torch.zeros(64 * 8, dtype=torch.uint8), i32.view(4, 16), 16,
+                        argmax=i32, max_logit=torch.zeros(64, dtype=torch.float64))
+    with pytest.raises(ValueError, match="target"):
+        hdf.accept_keys(torch.zeros(64 * 8, dtype=torch.uint8), i32.view(4, 16).long(), 16,
+                        argmax=i32)
+    with pytest.raises(ValueError, match="accept_len"):
+        hdf.accept(i32.view(4, 16), i32.view(4, 16),
+                   out=(torch.zeros(3, dtype=torch.int32), i32[:4], i32[:5], i32))
+    with pytest.raises(ValueError, match="draft"):
+        hdf.accept(i32.view(4, 16).float(), i32.view(4, 16))
+    H = torch.zeros((2, 4, 64), dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="b_g"):
+        hdf.hc_reduce(H, torch.zeros((4, 256), dtype=torch.bfloat16), torch.zeros(4, dtype=torch.bfloat16))
+    with pytest.raises(ValueError, match="W_g"):
+        hdf.hc_reduce(H, torch.zeros((4, 256), dtype=torch.float32), torch.zeros(4))
+    with pytest.raises(ValueError, match="Y"):
+        hdf.hc_reduce(H, torch.zeros((4, 256), dtype=torch.bfloat16), torch.zeros(4),
+                      Y=torch.zeros((1, 64), dtype=torch.bfloat16))
