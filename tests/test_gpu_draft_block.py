@@ -73,6 +73,18 @@ def test_block_of_one():
     _compare(DraftCase(wl, [100, 7], [100, 7], B=1, sub=3))
 
 
+def test_largest_block_and_ragged_query_groups():
+    """B = 64, the largest block (four 16-query groups; the block's key tile is all valid
+    keys), and B = 33 (a last query group of one query), at head dims 64 and 128."""
+    wl = synth.small_bf16()
+    _compare(DraftCase(wl, [200, 70], [30, 70], B=64, sub=31))
+    _compare(DraftCase(wl, [129, 1, 600], [129, 1, 16], B=33, sub=32))
+    wl.drafter = synth.DrafterShape(d=512, n_layers=1, n_heads=4, head_dim=128, d_ff=1024,
+                                    vocab=1000)
+    wl.d = 512
+    _compare(DraftCase(wl, [300, 64], [40, 64], B=64, sub=33))
+
+
 def test_head_dim_128_and_loose_max_ctx():
     wl = synth.small_bf16()
     wl.drafter = synth.DrafterShape(d=512, n_layers=1, n_heads=4, head_dim=128, d_ff=1024,
