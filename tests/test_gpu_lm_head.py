@@ -85,6 +85,25 @@ def test_ragged_batch_rows():
     torch.cuda.empty_cache()
 
 
+def test_rows_past_one_launch():
+    """More rows than one launch takes (2^20; the row offsets of a launch stay in int32
+    tile arithmetic): 2^20 + 300 rows of d = 64, V = 129, no logits; the rows around the
+    boundary, the first and last rows and 500 others against the oracle, and the keys
+    handed back zeroed for the next call."""
+    M = (1 << 20) + 300
+    hid, w = _inputs(M, 64, 129, "bf16", 65)
+    rng = np.random.default_rng(65)
+    edge = [0, 1, M - 2, M - 1] + list(range((1 << 20) - 3, (1 << 20) + 3))
+    rows = sorted(set(edge) | set(rng.choice(M, 500, replace=False).tolist()))
+    _check(hid, w, rows=rows, want_logits=False)
+    ws = torch.zeros(hdf.lm_head_workspace(M, 129), dtype=torch.uint8, device="cuda")
+    hdf.lm_head_argmax(hid, hdf.pack_weight(w), ws=ws)
+    torch.cuda.synchronize()
+    assert int(torch.count_nonzero(ws)) == 0
+    del hid, ws
+    torch.cuda.empty_cache()
+
+
 def test_ties_take_lowest_index():
     d, V = 128, 3000
     hid, w = _inputs(4, d, V, "bf16", 63)
