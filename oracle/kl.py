@@ -20,6 +20,7 @@ from __future__ import annotations
 
 import numpy as np
 
+from .lm_head import lm_head_logits
 from .numerics import as_f64, rmsnorm, store
 
 
@@ -55,7 +56,7 @@ def kl_forward(H_pos, gamma, eps, w_lm, student_logits, labels, *, P: int, T: fl
     H_pos = np.asarray(H_pos)
     n = H_pos.shape[0]
     h = teacher_hidden(H_pos.reshape((n * P,) + H_pos.shape[2:]), gamma, eps, dtype)
-    t = h @ as_f64(w_lm).T                                       # teacher logits, [n*P, V]
+    t = lm_head_logits(h, w_lm)                                  # teacher logits, [n*P, V]
     z = as_f64(student_logits)
     B = z.shape[1]
     kl = kl_rows(t, z[:, 1:P + 1].reshape(n * P, -1), T).reshape(n, P)

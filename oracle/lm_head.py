@@ -13,9 +13,28 @@ import numpy as np
 from .numerics import as_f64
 
 
+_CHUNK = 8192   # vocabulary rows decoded at a time
+
+
 def lm_head_logits(hidden, w_lm) -> np.ndarray:
-    """[M, d] x [V, d]^T -> float64 logits [M, V]."""
-    return as_f64(hidden) @ as_f64(w_lm).T
+    """[M, d] x [V, d]^T -> float64 logits [M, V].  bf16 weights (uint16 bits) are
+    decoded to float64 a block of vocabulary rows at a time into one reused buffer, so
+    the full-vocabulary matrix never exists in float64 (4.2 GB at V = 129280, d = 4096);
+    every logit is the same float64 dot product either way."""
+    h = as_f64(hidden)
+    w = np.asarray(w_lm)
+    if w.dtype != np.uint16:
+        return h @ as_f64(w).T
+    V, d = w.shape
+    z = np.empty((h.shape[0], V), dtype=np.float64)
+    bits = np.empty((min(_CHUNK, V), d), dtype=np.uint32)
+    wf = np.empty((min(_CHUNK, V), d), dtype=np.float64)
+    for c0 in range(0, V, _CHUNK):
+        n = min(_CHUNK, V - c0)
+        np.left_shift(w[c0:c0 + n], 16, out=bits[:n], dtype=np.uint32)   # bf16 -> fp32 bits
+        wf[:n] = bits[:n].view(np.float32)
+        z[:, c0:c0 + n] = h @ wf[:n].T
+    return z
 
 
 def lm_head_argmax(hidden, w_lm):

@@ -22,7 +22,6 @@ import oracle.drafter as od
 import oracle.numerics as nm
 from oracle.drafter import Weights, draft_block
 from oracle.lm_head import lm_head_argmax
-from oracle.numerics import as_f64
 from tests._tol import E2E_LOGIT_ABS, E2E_MARGIN, STATE_RMS_REL
 
 
@@ -80,7 +79,7 @@ def test_bf16_chain_spread_at_full_size(monkeypatch):
     ys = [b(synth.reduced_states(wl, n, sub=s)) for s in range(n_seq)]
     toks = b(synth.block_tokens(wl))
     ref = draft_block(W, ys, toks, kv_prefix=pre)
-    w_lm = as_f64(wb["w_lm"])          # decoded once for both LM-head passes
+    w_lm = wb["w_lm"]                  # bf16 bits: the oracle decodes them a block at a time
     am0, lg0, mg0 = lm_head_argmax(ref, w_lm)
     rng = np.random.default_rng(0)
     orig = nm.store
