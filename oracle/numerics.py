@@ -17,7 +17,8 @@ _KEEP_MASK = np.uint64(~((1 << _DROP) - 1) & 0xFFFFFFFFFFFFFFFF)
 
 def decode_bf16(bits: np.ndarray) -> np.ndarray:
     """uint16 bf16 bit patterns -> float64 values (exact)."""
-    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32)
+    b <<= np.uint32(16)                      # in place: one temporary, not two
     return b.view(np.float32).astype(np.float64)
 
 
