@@ -228,7 +228,7 @@ def decode_leg(torch, synth, hdf, rounds, warmup):
     def targets(drafts):
         r = rnd[0]
         rnd[0] += 1
-        tgt[r, :, :B - 1].copy_(torch.where(keep[r], drafts, other[r]))
+        torch.where(keep[r], drafts, other[r], out=tgt[r, :, :B - 1])   # one kernel
         return tgt[r]
 
     def decoder():
