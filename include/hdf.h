@@ -382,16 +382,25 @@ hdf_status hdf_accept_keys(void* ws, int n_seq, int B, int32_t* argmax, float* m
                            int32_t* commit_offsets, int32_t* commit_tokens, hdf_stream_t stream);
 
 /* Context growth after a round (Sec. 1: the n_s accepted drafts and the target's token
- * after them join the context; Sec. 3.4: tau = n_s + 1): for every s,
- *   ctx_len[s]    += accept_len[s] + 1
- *   new_counts[s]  = accept_len[s] + 1          (skipped when new_counts is NULL)
- * accept_len  [n_seq] int32 (device): hdf_accept's output
- * ctx_len     [n_seq] int32 (device, in/out); new_counts [n_seq] int32 (device, out)
- * The next round's hdf_draft_block_paged takes ctx_len and new_counts as they are,
- * with no host read in between.  The caller keeps max_ctx and the page table ahead of
- * the growth (at most B positions a round with B = K + 1). */
+ * after them join the context, and that token anchors the next block; Sec. 3.4:
+ * tau = n_s + 1): for every s,
+ *   ctx_len[s]        += accept_len[s] + 1
+ *   new_counts[s]      = accept_len[s] + 1      (skipped when new_counts is NULL)
+ *   block_tokens[s*B]  = next_anchor[s]         (skipped when block_tokens is NULL)
+ * accept_len   [n_seq] int32 (device): hdf_accept's output
+ * ctx_len      [n_seq] int32 (device, in/out); new_counts [n_seq] int32 (device, out)
+ * next_anchor  [n_seq] int32 (device): hdf_accept's output; required with block_tokens
+ * block_tokens [n_seq][B] int32 (device, in/out): the next round's block tokens; only
+ *              slot 0 of each row is written (the mask slots stay)
+ * B            the block size, 1 <= B <= 1025, when block_tokens is given (else ignored)
+ * The next round's hdf_draft_block_paged takes ctx_len, new_counts and block_tokens as
+ * they are, with no host read in between.  The caller keeps max_ctx and the page table
+ * ahead of the growth (at most B positions a round with B = K + 1).
+ * Errors: HDF_E_INVALID for n_seq < 0, null accept_len / ctx_len, block_tokens without
+ * next_anchor or B outside [1, 1025]; HDF_E_UNSUPPORTED when n_seq * B >= 2^31. */
 hdf_status hdf_advance_context(int n_seq, const int32_t* accept_len, int32_t* ctx_len,
-                               int32_t* new_counts, hdf_stream_t stream);
+                               int32_t* new_counts, const int32_t* next_anchor,
+                               int32_t* block_tokens, int B, hdf_stream_t stream);
 
 /* ------------------------------------------------------------------------------
  * 5. Temperature sampling and speculative-sampling verification (the temperature-1

@@ -757,11 +757,20 @@ hdf_status hdf_draft_block_paged(const hdf_drafter* w, int n_seq, int B, const i
 }
 
 hdf_status hdf_advance_context(int n_seq, const int32_t* accept_len, int32_t* ctx_len,
-                               int32_t* new_counts, hdf_stream_t stream) {
+                               int32_t* new_counts, const int32_t* next_anchor,
+                               int32_t* block_tokens, int B, hdf_stream_t stream) {
   if (n_seq < 0) return fail(HDF_E_INVALID, "advance_context: n_seq < 0");
   if (n_seq > 0 && (accept_len == nullptr || ctx_len == nullptr))
     return fail(HDF_E_INVALID, "advance_context: null accept_len/ctx_len");
+  if (block_tokens != nullptr) {
+    if (next_anchor == nullptr)
+      return fail(HDF_E_INVALID, "advance_context: block_tokens given without next_anchor");
+    if (B < 1 || B > 1025) return fail(HDF_E_INVALID, "advance_context: B=%d outside [1, 1025]", B);
+    if (int64_t(n_seq) * B > INT32_MAX)
+      return fail(HDF_E_UNSUPPORTED, "advance_context: n_seq*B exceeds int32 offsets");
+  }
   const hipError_t e = hdf::launch_advance_context(n_seq, accept_len, ctx_len, new_counts,
+                                                   next_anchor, block_tokens, B,
                                                    reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "advance_context launch");
   return ok();

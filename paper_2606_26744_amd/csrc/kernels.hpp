@@ -151,7 +151,8 @@ struct PrepArgs {
 hipError_t launch_prep(bool bf16, const PrepArgs& a, hipStream_t s);
 // ctx_len[s] += accept_len[s] + 1; new_counts[s] = accept_len[s] + 1 (new_counts may be NULL)
 hipError_t launch_advance_context(int n_seq, const int32_t* accept_len, int32_t* ctx_len,
-                                  int32_t* new_counts, hipStream_t s);
+                                  int32_t* new_counts, const int32_t* next_anchor,
+                                  int32_t* block_tokens, int B, hipStream_t s);
 // h += sum_z parts[z]; u = RMSNorm(h) * gamma
 hipError_t launch_residual_norm(bool bf16, const float* parts, int S, const float* gamma, float eps,
                                 int64_t rows, int d, float* h, void* u, hipStream_t s);

@@ -279,21 +279,25 @@ hipError_t launch_prep(bool bf16, const PrepArgs& a, hipStream_t s) {
 
 // After a verification round: sequence s committed accept_len[s] + 1 positions (its
 // accepted drafts and the target's token after them), which become its newest context
-// rows for the next round.
+// rows for the next round; that token is the next block's anchor (slot 0).
 __global__ void advance_context_kernel(int n_seq, const int32_t* __restrict__ accept_len,
-                                       int32_t* __restrict__ ctx_len, int32_t* __restrict__ new_counts) {
+                                       int32_t* __restrict__ ctx_len, int32_t* __restrict__ new_counts,
+                                       const int32_t* __restrict__ next_anchor,
+                                       int32_t* __restrict__ block_tokens, int B) {
   const int s = blockIdx.x * blockDim.x + threadIdx.x;
   if (s >= n_seq) return;
   const int n = accept_len[s] + 1;
   ctx_len[s] += n;
   if (new_counts != nullptr) new_counts[s] = n;
+  if (block_tokens != nullptr) block_tokens[int64_t(s) * B] = next_anchor[s];
 }
 
 hipError_t launch_advance_context(int n_seq, const int32_t* accept_len, int32_t* ctx_len,
-                                  int32_t* new_counts, hipStream_t s) {
+                                  int32_t* new_counts, const int32_t* next_anchor,
+                                  int32_t* block_tokens, int B, hipStream_t s) {
   if (n_seq <= 0) return hipSuccess;
   hipLaunchKernelGGL(advance_context_kernel, dim3(unsigned((n_seq + 255) / 256)), dim3(256), 0, s,
-                     n_seq, accept_len, ctx_len, new_counts);
+                     n_seq, accept_len, ctx_len, new_counts, next_anchor, block_tokens, B);
   return hipGetLastError();
 }
 

@@ -270,8 +270,8 @@ class PagedDecoder:
                         "ctx_len": self.chain_ctx.clone()})
         acc, anc, offs, toks = hdf.accept(am[1:], tg, K=B - 1, draft_stride=B,
                                           out=(self.acc, self.anc, self.offs, self.toks))
-        self.tokens[:, 0] = anc
-        hdf.advance_context(acc, self.chain_ctx, self.chain_counts)
+        hdf.advance_context(acc, self.chain_ctx, self.chain_counts, next_anchor=anc,
+                            block_tokens=self.tokens)
         # the lengths after this round, read back without waiting
         k = self._rb_slot
         if any(slot == k for _, slot, _ in self._rb_pending):

@@ -98,7 +98,7 @@ def lib() -> ctypes.CDLL:
     L.hdf_kv_read_rows.restype = _I
     L.hdf_kv_read_rows.argtypes = [_P, _P, _I64, _I, _I, _I, _I, _P, _I64, _I64, _P, _P, _P]
     L.hdf_advance_context.restype = _I
-    L.hdf_advance_context.argtypes = [_I, _P, _P, _P, _P]
+    L.hdf_advance_context.argtypes = [_I, _P, _P, _P, _P, _P, _I, _P]
     L.hdf_fc_reduce_workspace.restype = _SZ
     L.hdf_fc_reduce_workspace.argtypes = [_I64, _I, _I, _I]
     L.hdf_fc_reduce.restype = _I
@@ -249,15 +249,27 @@ def accept(draft: torch.Tensor, target: torch.Tensor, *, K: Optional[int] = None
 
 
 def advance_context(accept_len: torch.Tensor, ctx_len: torch.Tensor,
-                    new_counts: Optional[torch.Tensor] = None, stream=None):
+                    new_counts: Optional[torch.Tensor] = None, stream=None,
+                    next_anchor: Optional[torch.Tensor] = None,
+                    block_tokens: Optional[torch.Tensor] = None):
     """hdf_advance_context: ctx_len += accept_len + 1 and new_counts = accept_len + 1, on
-    the device (int32 [n_seq] tensors; ctx_len in place)."""
+    the device (int32 [n_seq] tensors; ctx_len in place); with block_tokens (int32
+    [n_seq, B], contiguous) also block_tokens[s, 0] = next_anchor[s]."""
     n_seq = ctx_len.shape[0]
-    for t in (accept_len, ctx_len, new_counts):
+    for t in (accept_len, ctx_len, new_counts, next_anchor):
         if t is not None and (t.dtype != torch.int32 or t.numel() != n_seq):
             raise ValueError("advance_context takes int32 [n_seq] tensors")
-    _dev(accept_len, ctx_len, new_counts)
+    B = 0
+    if block_tokens is not None:
+        if next_anchor is None:
+            raise ValueError("advance_context: block_tokens needs next_anchor")
+        if (block_tokens.dtype != torch.int32 or block_tokens.dim() != 2
+                or block_tokens.shape[0] != n_seq or not block_tokens.is_contiguous()):
+            raise ValueError("advance_context: block_tokens must be contiguous int32 [n_seq, B]")
+        B = block_tokens.shape[1]
+    _dev(accept_len, ctx_len, new_counts, next_anchor, block_tokens)
     _check(lib().hdf_advance_context(n_seq, _ptr(accept_len), _ptr(ctx_len), _ptr(new_counts),
+                                     _ptr(next_anchor), _ptr(block_tokens), B,
                                      _stream(stream)))
 
 

@@ -187,13 +187,21 @@ def test_draft_block_paged_validation():
 
 
 def test_advance_context_validation():
-    """Null inputs and a negative count are rejected on the host; n_seq = 0 is a no-op."""
+    """Null inputs, a negative count, block tokens without anchors and a block size outside
+    [1, 1025] are rejected on the host; n_seq = 0 is a no-op."""
     L = hdf.lib()
     fake = ctypes.c_void_p(4096)
-    assert _status(L.hdf_advance_context(-1, fake, fake, fake, None)) == "HDF_E_INVALID"
-    assert _status(L.hdf_advance_context(2, None, fake, fake, None)) == "HDF_E_INVALID"
-    assert _status(L.hdf_advance_context(2, fake, None, None, None)) == "HDF_E_INVALID"
-    assert _status(L.hdf_advance_context(0, None, None, None, None)) == "HDF_OK"
+
+    def call(n, acc, ctx, anchor=None, toks=None, B=0):
+        return _status(L.hdf_advance_context(n, acc, ctx, fake, anchor, toks, B, None))
+    assert call(-1, fake, fake) == "HDF_E_INVALID"
+    assert call(2, None, fake) == "HDF_E_INVALID"
+    assert call(2, fake, None) == "HDF_E_INVALID"
+    assert call(2, fake, fake, None, fake, 16) == "HDF_E_INVALID"     # tokens need anchors
+    assert call(2, fake, fake, fake, fake, 0) == "HDF_E_INVALID"
+    assert call(2, fake, fake, fake, fake, 1026) == "HDF_E_INVALID"
+    assert call(1 << 22, fake, fake, fake, fake, 1024) == "HDF_E_UNSUPPORTED"
+    assert call(0, None, None) == "HDF_OK"
 
 
 def test_fc_reduce_validation():
