@@ -632,7 +632,7 @@ static hdf_status draft_block_impl(const hdf_drafter* w, int n_seq, int B, const
       // Rows d..3d-1 (W_k; W_v) of the packed W_qkv: d/128 whole row groups in.
       const char* wkv = static_cast<const char*>(w->w_qkv[l]) + size_t(d) * d * el;
       const hdf::GemmPlan Sp = hdf::gemm_plan(bf, rows, 2 * d, d);
-      if (bf && Sp.tn == 2 && Sp.nw == 8 && Sp.splits == 1 && (hd == 64 || hd == 128) &&
+      if (bf && Sp.tn == 4 && Sp.nw == 4 && Sp.splits == 1 && (hd == 64 || hd == 128) &&
           d % 512 == 0) {
         // One K split: RoPE and the cache stores happen in the GEMM's epilogue, so the
         // fp32 rows never go through memory.

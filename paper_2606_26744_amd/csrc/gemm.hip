@@ -10,12 +10,14 @@
 // with one contiguous 1 KB load per instruction, the four waves of a workgroup read
 // one contiguous 16 KB run per 64-k step, and no weight byte passes through LDS.
 //
-// bf16 kernel: NW waves (4, 6 or 8), each owning TN 32-column blocks (1, or 2 for the
-// matrix-core bound shapes and the LM head) and all BM rows (BM = 128, or 64 when
-// M <= 64) of a 32*NW*TN-column tile.  The activation slice (BM x 64) is shared
-// through a double-buffered, padded LDS tile.  A ring of STAGES K-steps of weights is
-// in flight per wave; activations are fetched one step further ahead than weights
-// because memory counters complete in issue order.
+// bf16 kernel: NW waves (4, 6 or 8), each owning TN 32-column blocks (1; 2 for the LM
+// head's 128-row weight stream; 4 for the matrix-core bound shapes) and all BM rows
+// (BM = 128, or 64 when M <= 64) of a 32*NW*TN-column tile.  The activation slice
+// (BM x 64) is shared through a double-buffered, padded LDS tile.  A ring of STAGES
+// K-steps of weights is in flight per wave; activations are fetched one step further
+// ahead than weights because memory counters complete in issue order.  The matrix-core
+// bound tiles (128 x 512, 4 waves of 4 x 4 blocks, one wave per SIMD) run the deep K loop
+// described at its code.
 // Split-K runs over gridDim.z; tiles are ordered so that the M-tiles of one weight
 // column block run on the same XCD back to back (its L2 serves the re-reads); in tall
 // matrix-core bound problems an XCD's concurrent tiles form 8 x 4 blocks of row and column
@@ -60,16 +62,25 @@ __device__ __forceinline__ unsigned long long argmax_key(float v, int col) {
          static_cast<unsigned long long>(0xFFFFFFFFu - static_cast<uint32_t>(col));
 }
 
-// TN: 32-column weight blocks per wave (1 or 2).  Each activation fragment read from
-// LDS feeds TN matrix-core operations, so TN = 2 halves the LDS traffic per MFMA; the
+// Activation unit of the deep K loop in LDS: row r's four 16-byte chunks (8 of K each)
+// sit at chunk positions c ^ unit_swizzle(r), so that the row-wise stores (four threads
+// a row) and the fragment reads (32 rows, one chunk each) meet distinct banks.
+__device__ __forceinline__ int unit_swizzle(int r) { return ((r >> 1) ^ (r >> 2)) & 3; }
+
+// TN: 32-column weight blocks per wave (1, 2 or 4).  Each activation fragment read from
+// LDS feeds TN matrix-core operations, so wider waves cut the LDS traffic per MFMA; the
 // compute-bound shapes (a few hundred rows and more) need it, the weight streams of
 // 128 rows prefer more waves per CU instead.
 // NT: fetch the weights with non-temporal loads (they stream past the caches).  Right
 // when one row tile reads every weight byte once; with several row tiles the others
 // re-read the weights from L2, so they are fetched through the caches.
-// PP: the ping-pong K loop of the matrix-core bound tiles (128 x 512, 8 waves of two
-// blocks): the two waves of a SIMD alternate between a memory phase and a compute phase.
-template <int BM, int NW, int STAGES, int EPI, int TN = 1, bool NT = (TN == 1), bool PP = false>
+// PP: the ping-pong K loop (128 x 512 tiles, 8 waves of two blocks): the two waves of a
+// SIMD alternate between a memory phase and a compute phase.  The K/V and argmax
+// epilogues of the matrix-core bound shapes run on it.
+// DEEP: the K loop of the matrix-core bound partial-sum tiles (128 x 512, 4 waves of 4 x 4
+// blocks, one wave per SIMD, a STAGES-unit weight ring in registers).
+template <int BM, int NW, int STAGES, int EPI, int TN = 1, bool NT = (TN == 1), bool PP = false,
+          bool DEEP = false>
 __global__ void __launch_bounds__(NW * 64)
 gemm_bf16_kernel(GemmArgs p) {
   constexpr int THREADS = NW * 64;
@@ -84,9 +95,12 @@ gemm_bf16_kernel(GemmArgs p) {
   // LDS: the activation buffers, reused after the K loop by the K/V epilogue and the
   // ARGMAX epilogue's logits to stage the fp32 tile 128 columns at a time ([block][row]
   // [32 columns]), and by the ARGMAX epilogue's per-wave row maxima.
-  constexpr size_t kMainLds = PP ? size_t(4) * BM * (32 + 8) * sizeof(bf16_t)   // NBUF units
-                                : size_t(2) * BM * LDA * sizeof(bf16_t);
-  constexpr size_t kEpiLds = (EPI != kEpiPartial) ? size_t(4) * BM * LDC * sizeof(float) : 0;
+  constexpr size_t kMainLds = PP     ? size_t(4) * BM * (32 + 8) * sizeof(bf16_t)   // NBUF units
+                              : DEEP ? size_t(2) * BM * 32 * sizeof(bf16_t)          // two K units
+                                     : size_t(2) * BM * LDA * sizeof(bf16_t);
+  constexpr size_t kEpiLds = (EPI != kEpiPartial)
+      ? size_t(4) * BM * LDC * sizeof(float) + (EPI == kEpiKV ? size_t(2) * BM * sizeof(int) : 0)
+      : 0;
   __shared__ __attribute__((aligned(16))) unsigned char smem[kMainLds > kEpiLds ? kMainLds : kEpiLds];
   typedef bf16_t ATile[BM][LDA];
   ATile* As = reinterpret_cast<ATile*>(smem);
@@ -110,7 +124,7 @@ gemm_bf16_kernel(GemmArgs p) {
   }
   const int mt = (p.M + BM - 1) / BM;
   int n_tile = tile / mt, m_tile = tile % mt;
-  if (PP && mt > kGroupRows) {
+  if ((PP || DEEP) && mt > kGroupRows) {
     // Tall problems (the cold context projection): consecutive tile ids walk a group of
     // kGroupRows row tiles, then the next column block, so the 32 tiles an XCD runs at
     // once are 8 row tiles x 4 column blocks and share their activation and weight slices
@@ -252,6 +266,110 @@ gemm_bf16_kernel(GemmArgs p) {
         if (u + j < nu) unit(u + j, j);
       if (grp == 0) __syncthreads();   // group 0 ends one phase later
     }
+  } else if constexpr (DEEP) {
+    // One wave per SIMD.  Each wave owns all 128 rows and one 128-row weight group (4 x 4
+    // blocks of 32 x 32), so every activation fragment read from LDS feeds four MFMAs and
+    // the 512 accumulators fill the accumulation registers.  A unit is 32 of K (two MFMA
+    // sub-steps).  The weights of a unit (8 KB a wave, 1 KB per load) go straight into a
+    // ring of R register slots, issued D = R - 1 units before their MFMAs.  The
+    // activations come through two swizzled LDS unit buffers: a thread stores its share
+    // of unit u+1 in the first half of unit u, one workgroup barrier follows, and the
+    // fragments of unit u+1's first sub-step are read during the second half, those of its
+    // second sub-step during the first half of unit u+1.  Loads are issued in the order
+    // they are waited for (the activations of unit u+D+1, then the weights of unit u+D),
+    // so the in-order load counter never makes one wait for the other.
+    static_assert(BM == 128 && NW == 4 && TN == 4, "deep tiles are 128 x 512, 4 waves of 4 x 4 blocks");
+    constexpr int UK = 32;
+    constexpr int R = STAGES;
+    constexpr int D = R - 1;
+    typedef bf16_t UTile[BM * UK];
+    UTile* Au = reinterpret_cast<UTile*>(smem);
+    const int nu = nk * (kBK / UK);
+    const int64_t ku0 = int64_t(kt_begin) * (kBK / UK);
+    // Activation staging: 512 chunks of 16 bytes per unit, thread tid moves chunks tid and
+    // tid + 256 (row q/4, chunk q%4).  Rows past M are clamped, units past the end re-read
+    // the last one; neither is ever used.
+    const bf16_t* a_src[2];
+    int a_lds[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int q = tid + 256 * j, row = q >> 2, c = q & 3;
+      a_src[j] = A + int64_t(min(m0 + row, p.M - 1)) * p.lda + c * 8;
+      a_lds[j] = row * UK + ((c ^ unit_swizzle(row)) * 8);
+    }
+    // Fragment of sub-step ss, row block i: lane l reads row 32i + l%32, chunk 2ss + l/32.
+    const int fr = lane & 31;
+    int f_off[2];
+#pragma unroll
+    for (int ss = 0; ss < 2; ++ss) f_off[ss] = fr * UK + (((2 * ss + (lane >> 5)) ^ unit_swizzle(fr)) * 8);
+    auto a_load = [&](int u, u32x4* dst) {
+      const int64_t k = (ku0 + min(u, nu - 1)) * UK;
+      dst[0] = ld16(a_src[0] + k);
+      dst[1] = ld16(a_src[1] + k);
+    };
+    auto a_store = [&](const u32x4* src, int buf) {
+      *reinterpret_cast<u32x4*>(&Au[buf][a_lds[0]]) = src[0];
+      *reinterpret_cast<u32x4*>(&Au[buf][a_lds[1]]) = src[1];
+    };
+    // Units past the end are never used: their loads read the activations' first 16
+    // bytes (in L2) instead of the weights.
+    auto b_load = [&](int u, u32x4 (*dst)[TN]) {
+      const bool live = u < nu;
+      const int64_t kb = (ku0 + (live ? u : 0)) * (UK / 16);
+#pragma unroll
+      for (int ss = 0; ss < 2; ++ss)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn)
+          dst[ss][tn] = ld16(live ? Bw[tn] + (kb + ss) * 4 * 512 : A);
+    };
+    auto frag = [&](int buf, int ss, int i) {
+      return *reinterpret_cast<const bf16x8_t*>(&Au[buf][f_off[ss] + 32 * i * UK]);
+    };
+    if (nu > 0) {
+      u32x4 rb[R][2][TN];
+      u32x4 ra[R][2];
+      a_load(0, ra[0]);
+#pragma unroll
+      for (int x = 0; x < D; ++x) {
+        a_load(x + 1, ra[(x + 1) % R]);
+        b_load(x, rb[x]);
+      }
+      a_store(ra[0], 0);
+      lds_barrier();
+      bf16x8_t f0[TM], f1[TM];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) f0[i] = frag(0, 0, i);
+      // Unit u in ring slot s = u % R.
+      auto unit = [&](int u, int s) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) f1[i] = frag(u & 1, 1, i);
+        a_store(ra[(u + 1) % R], (u + 1) & 1);
+        a_load(u + D + 1, ra[(u + D + 1) % R]);
+        b_load(u + D, rb[(s + D) % R]);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int tn = 0; tn < TN; ++tn)
+            acc[i][tn] = mma(f0[i], __builtin_bit_cast(bf16x8_t, rb[s][0][tn]), acc[i][tn]);
+        lds_barrier();
+#pragma unroll
+        for (int i = 0; i < TM; ++i) f0[i] = frag((u + 1) & 1, 0, i);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int tn = 0; tn < TN; ++tn)
+            acc[i][tn] = mma(f1[i], __builtin_bit_cast(bf16x8_t, rb[s][1][tn]), acc[i][tn]);
+      };
+      int u = 0;
+      for (; u + R <= nu; u += R) {
+#pragma unroll
+        for (int j = 0; j < R; ++j) unit(u + j, j);
+      }
+#pragma unroll
+      for (int j = 0; j < R; ++j)
+        if (u + j < nu) unit(u + j, j);
+    }
+    lds_barrier();   // the epilogues reuse LDS
   } else if (nk > 0) {
     u32x4 ra[STAGES][A_CH];
     u32x4 rb[STAGES][TN * 4];
@@ -361,12 +479,44 @@ gemm_bf16_kernel(GemmArgs p) {
     // consecutive threads on consecutive rows of one dim.  The same fp32 values and the
     // same rounding as the partial-sum path and its epilogue kernel.
     float* Cs = reinterpret_cast<float*>(smem);
+    // The tile's row table: cache row (-1: not stored) and position of every row, read
+    // once here so that no store below waits on a dependent global load.
+    int* rtab = reinterpret_cast<int*>(Cs + 4 * BM * LDC);
+    int* ptab = rtab + BM;
     const bool is_v = n0 >= p.kv_d;
     const int HD = p.hd, HALF = HD >> 1;
+    if (tid < BM) {
+      const int row = m0 + tid;
+      const int dr = row < p.M ? p.plan_row[row] : -1;
+      rtab[tid] = dr;
+      ptab[tid] = dr >= 0 ? p.plan_pos[row] : 0;
+    }
     auto at = [&](int rr, int cc) { return Cs[((cc >> 5) * BM + rr) * LDC + (cc & 31)]; };
+    // K items (row, octet of eight rotated pairs): 8 octets per row of a slab, each stored
+    // as two 16-byte runs (dims i0..i0+7 and i0+hd/2..i0+hd/2+7 are contiguous in the key
+    // tile layout).  A thread's items are rows rr, rr + THREADS/8, ... of one octet, the
+    // same rows and dims in every slab, so their rotation-table entries are fetched once
+    // per tile, before the first slab (rows without a cache row fetch entry 0 and are
+    // skipped).  The barriers below order LDS traffic only, so the stores of one slab
+    // stay in flight while the next one is staged.
+    constexpr int KI = BM * 8 / THREADS;
+    static_assert(KI * THREADS == BM * 8, "whole items per thread");
+    const int oc = tid & 7;
+    const int kj = (8 * oc) / HALF;           // head inside the slab
+    const int i0 = 8 * oc - kj * HALF;
+    float4 cs[KI][4];
+    lds_barrier();                             // the row table
+    if (!is_v && p.rope_cs != nullptr) {
+#pragma unroll
+      for (int it = 0; it < KI; ++it) {
+        const float* c = p.rope_cs + (int64_t(ptab[(tid >> 3) + it * (THREADS / 8)]) * HALF + i0) * 2;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) cs[it][q] = *reinterpret_cast<const float4*>(c + 4 * q);
+      }
+    }
 #pragma unroll 1
     for (int slab = 0; slab < NB / 4; ++slab) {
-      if (slab > 0) __syncthreads();
+      if (slab > 0) lds_barrier();
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) {
         const int b = wid * TN + tn;
@@ -380,21 +530,16 @@ gemm_bf16_kernel(GemmArgs p) {
             }
         }
       }
-      __syncthreads();
+      lds_barrier();
       const int c0 = n0 + 128 * slab - (is_v ? p.kv_d : 0);   // slab start inside K or V
       if (c0 >= p.kv_d) continue;                             // columns past N
       if (!is_v) {
-        // Items (row, octet of eight rotated pairs): 8 octets per row of the slab, each
-        // stored as two 16-byte runs (dims i0..i0+7 and i0+hd/2..i0+hd/2+7 are contiguous
-        // in the key tile layout).
-        for (int e = tid; e < BM * 8; e += THREADS) {
-          const int rr = e >> 3, oc = e & 7;
-          const int row = m0 + rr;
-          if (row >= p.M) continue;
-          const int drow = p.plan_row[row];
+        const int j = kj;
+#pragma unroll
+        for (int it = 0; it < KI; ++it) {
+          const int rr = (tid >> 3) + it * (THREADS / 8);
+          const int drow = rtab[rr];
           if (drow < 0) continue;
-          const int j = (8 * oc) / HALF;        // head inside the slab
-          const int i0 = 8 * oc - j * HALF;
           float y1[8], y2[8];
 #pragma unroll
           for (int k = 0; k < 8; ++k) {
@@ -402,12 +547,10 @@ gemm_bf16_kernel(GemmArgs p) {
             y2[k] = at(rr, j * HD + HALF + i0 + k);
           }
           if (p.rope_cs != nullptr) {
-            const float* cs = p.rope_cs + (int64_t(p.plan_pos[row]) * HALF + i0) * 2;
 #pragma unroll
-            for (int k = 0; k < 8; k += 2) {
-              const float4 c = *reinterpret_cast<const float4*>(cs + 2 * k);
-              rope_rotate(y1[k], y2[k], c.x, c.y);
-              rope_rotate(y1[k + 1], y2[k + 1], c.z, c.w);
+            for (int q = 0; q < 4; ++q) {
+              rope_rotate(y1[2 * q], y2[2 * q], cs[it][q].x, cs[it][q].y);
+              rope_rotate(y1[2 * q + 1], y2[2 * q + 1], cs[it][q].z, cs[it][q].w);
             }
           }
           bf16_t* kh = static_cast<bf16_t*>(p.kc) + int64_t(c0 / HD + j) * p.cap * HD;
@@ -429,10 +572,10 @@ gemm_bf16_kernel(GemmArgs p) {
           const int col = c0 + cc;
           bf16_t* vh = static_cast<bf16_t*>(p.vtc) + int64_t(col / HD) * p.cap * HD;
           const int i = col % HD;
-          const int d0 = p.plan_row[row0];
+          const int d0 = rtab[8 * rg];
           bool run = row0 + 8 <= p.M && d0 >= 0 && (d0 & 7) == 0;
 #pragma unroll
-          for (int k = 1; k < 8; ++k) run = run && p.plan_row[row0 + k] == d0 + k;
+          for (int k = 1; k < 8; ++k) run = run && rtab[8 * rg + k] == d0 + k;
           if (run) {
             float v[8];
 #pragma unroll
@@ -442,7 +585,7 @@ gemm_bf16_kernel(GemmArgs p) {
                            pack_bf2(v[6], v[7]));
           } else {
             for (int k = 0; k < 8 && row0 + k < p.M; ++k) {
-              const int dr = p.plan_row[row0 + k];
+              const int dr = rtab[8 * rg + k];
               if (dr >= 0) vh[vc_index(dr, i, HD)] = f2bf(at(8 * rg + k, cc));
             }
           }
@@ -472,11 +615,13 @@ gemm_bf16_kernel(GemmArgs p) {
         const int col = cb + 8 * (r >> 2) + (r & 3);
         const bool in = col < p.N;
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
-          if (in && acc[i][tn][r] > best[i]) {
-            best[i] = acc[i][tn][r];
-            bcol[i] = col;
-          }
+        for (int i = 0; i < TM; ++i) {
+          // selects, not branches: one compare and two conditional moves per value
+          const float v = acc[i][tn][r];
+          const bool take = in & (v > best[i]);
+          best[i] = take ? v : best[i];
+          bcol[i] = take ? col : bcol[i];
+        }
       }
     }
 #pragma unroll
@@ -662,7 +807,20 @@ __global__ void pack_weight_kernel(const T* __restrict__ src, T* __restrict__ ds
 
 // ---------------------------------------------------------------------------- host side
 
-template <int NW, int TN, int STAGES = 4, bool NT = (TN == 1), bool PP = (TN == 2)>
+// Matrix-core bound tiles: 128 x 512 in the deep K loop, 4 waves of 4 x 4 blocks with a
+// 4-unit weight ring (3 or 4 units measured the same; the register file holds no more).
+constexpr int kDeepWaves = 4, kDeepBlocks = 4, kDeepRing = 4;
+
+template <int EPI>
+static void launch_bf16_deep(const GemmArgs& a, int splits, hipStream_t s) {
+  constexpr int BN = 32 * kDeepWaves * kDeepBlocks;
+  const int tiles = ((a.M + 127) / 128) * ((a.N + BN - 1) / BN) +
+                    ((a.M2 + 127) / 128) * ((a.N2 + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_bf16_kernel<128, kDeepWaves, kDeepRing, EPI, kDeepBlocks, false, false, true>),
+                     dim3(tiles, 1, splits), dim3(kDeepWaves * 64), 0, s, a);
+}
+
+template <int NW, int TN, int STAGES = 4, bool NT = (TN == 1)>
 static void launch_bf16_partial(const GemmArgs& a, int splits, hipStream_t s) {
   const int BM = (a.M <= 64 && a.M2 <= 64) ? 64 : 128;
   constexpr int BN = 32 * NW * TN;
@@ -673,8 +831,8 @@ static void launch_bf16_partial(const GemmArgs& a, int splits, hipStream_t s) {
     hipLaunchKernelGGL((gemm_bf16_kernel<64, NW, STAGES, kEpiPartial, TN, NT>), grid, block, 0, s,
                        a);
   else
-    hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, STAGES, kEpiPartial, TN, NT, PP>), grid, block,
-                       0, s, a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<128, NW, STAGES, kEpiPartial, TN, NT>), grid, block, 0, s,
+                       a);
 }
 
 // One pass for 128 < M <= 256 rows: every row in one tile (192 or 256 rows), 8 waves of
@@ -714,8 +872,8 @@ static hipError_t launch_gemm_any(bool bf16, int epi, const GemmArgs& a, GemmPla
                                   hipStream_t s) {
   if (bf16) {
     if (epi == kEpiPartial) {
-      if (plan.tn == 2) {
-        launch_bf16_partial<8, 2, 2>(a, plan.splits, s);
+      if (plan.tn == kDeepBlocks) {
+        launch_bf16_deep<kEpiPartial>(a, plan.splits, s);
       } else if (!plan.nt) {
         launch_bf16_partial<8, 1, 4, false>(a, plan.splits, s);
       } else if (plan.nw == 8) {
@@ -770,7 +928,7 @@ GemmPlan gemm_plan2(bool bf16, int M, int N, int M2, int N2, int K) {
   const int BM = (M <= 64 && M2 <= 64) ? 64 : 128;
   const bool mfma_bound = M > 128 || M2 > 128;
   if (mfma_bound) {
-    // Matrix-core bound: 8 waves x 2 blocks (128 x 512 tiles).  The time is about the
+    // Matrix-core bound: the deep 128 x 512 tiles.  The time is about the
     // number of rounds of workgroups over the CUs times the K range of one workgroup,
     // plus the fp32 partials of every extra split (charged 15% each): pick the split
     // that minimises rounds / splits * (1 + 0.15 (splits - 1)).  At 1024 rows: gate/up
@@ -787,7 +945,7 @@ GemmPlan gemm_plan2(bool bf16, int M, int N, int M2, int N2, int K) {
         best_s = sp;
       }
     }
-    return GemmPlan{8, best_s, 2};
+    return GemmPlan{kDeepWaves, best_s, kDeepBlocks};
   }
   return plan_stream(BM, M, N, M2, N2, nk, ncu, {4, 6, 8});
 }
@@ -865,7 +1023,9 @@ hipError_t launch_gemm_kv(const void* A, int64_t lda, const void* B, int M, int 
                           GemmPlan plan, const int32_t* plan_pos, const int32_t* plan_row,
                           const float* rope_cs, void* kc, void* vtc, int64_t cap, hipStream_t s) {
   // 512-column tiles lie wholly in K or in V when d % 512 == 0.
-  if (plan.tn != 2 || plan.nw != 8 || plan.splits != 1 || (hd != 64 && hd != 128) ||
+  // The matrix-core bound plan with one K split; the K/V epilogue runs on the ping-pong
+  // tiles of the same 512 columns.
+  if (plan.tn != kDeepBlocks || plan.nw != kDeepWaves || plan.splits != 1 || (hd != 64 && hd != 128) ||
       d % 512 != 0)
     return hipErrorInvalidValue;
   if (M <= 0) return hipSuccess;

@@ -66,7 +66,7 @@ int gemm_k_align(bool bf16);                       // K must be a multiple of th
 // 4, 6 or 8) and the number of K splits.
 struct GemmPlan {
   int nw, splits;
-  int tn = 1;       // 32-column blocks per wave (2 for compute-bound shapes)
+  int tn = 1;       // 32-column blocks per wave (4 for the matrix-core bound shapes)
   bool nt = true;   // one-block waves: weights streamed past the caches
 };
 GemmPlan gemm_plan(bool bf16, int M, int N, int K);
