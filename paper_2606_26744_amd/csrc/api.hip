@@ -118,10 +118,11 @@ DraftPlan plan_workspace(const hdf_drafter& w, int n_seq, int B, int64_t n_new, 
   // (sequence, head) pair, a chunk is the longest power of two from 512 up that still
   // gives every CU a workgroup (at most 16384): 8 x 2048 positions take one chunk of
   // 2048 keys and need no merge.  Otherwise chunks are the longest power of two in
-  // [512, 8192] that still gives four workgroups per CU (each chunk costs a partial
-  // output and a merge): 8192 keys for 64 sequences of up to 16K positions (ragged step
-  // 3.82 -> 3.27 ms from 512 to 4096 keys with 4-wave workgroups, 3.22 -> 3.17 ms from
-  // those to 8-wave workgroups of 8192 keys).
+  // [512, 16384] that still gives four workgroups per CU (each chunk costs a partial
+  // output and a merge): one chunk of 16384 keys for 64 sequences of up to 16K positions
+  // (ragged step 3.82 -> 3.27 ms from 512 to 4096 keys with 4-wave workgroups, 3.22 ->
+  // 3.17 ms from those to 8-wave workgroups of 8192 keys, 3.01 -> 2.97 ms from 8192 keys
+  // and a merge to one chunk).
   {
     const int64_t pairs = int64_t(n_seq) * w.n_heads * ((B + 15) / 16);
     const int64_t cus = hdf::device_cu_count();
@@ -132,7 +133,7 @@ DraftPlan plan_workspace(const hdf_drafter& w, int n_seq, int B, int64_t n_new, 
     if (pairs * std::max<int64_t>(1, (max_ctx + c - 1) / c) > cus) {
       const int64_t per_wg = int64_t(n_seq) * max_ctx * w.n_heads / (int64_t(4) * cus);
       c = 512;
-      while (c < 8192 && 2 * c <= per_wg) c *= 2;
+      while (c < hdf::kAttnMaxChunk && 2 * c <= per_wg) c *= 2;
     }
     P.chunk_len = int(c);
   }
