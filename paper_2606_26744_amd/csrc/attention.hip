@@ -43,6 +43,7 @@ namespace hdf {
 constexpr int kCombineThreads = 256;
 constexpr int kKeyTile = 64;
 constexpr int kMaxChunkTiles = kAttnMaxChunk / kKeyTile;
+constexpr int kAttnSortSeqs = 1024;   // longest-context-first dispatch up to this many sequences
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -67,15 +68,38 @@ attn_bf16_kernel(AttnArgs a, bf16_t* __restrict__ out) {
   __shared__ float red_l[kAttnWaves][16];
   __shared__ int64_t ctile[kMaxChunkTiles];   // cache tile of each context tile of the chunk
 
-  // Grid (head, sequence x query group, chunk): every sequence's first chunk is dispatched
-  // before any second chunk, and the blocks' own workgroups (a few keys each) come last,
-  // so the long chunks do not trail the launch (ragged 64-sequence step 3.03 -> 3.01 ms
-  // against chunk-fastest order).
+  // Grid (head, sequence slot x query group, chunk): every sequence's first chunk is
+  // dispatched before any second chunk, and the blocks' own workgroups (a few keys each)
+  // come last, so the long chunks do not trail the launch (ragged 64-sequence step 3.03 ->
+  // 3.01 ms against chunk-fastest order).  When the launch is more than two rounds of
+  // workgroups, sequence slot j takes the sequence with the j-th longest context (ties by
+  // index), so that the dispatch runs longest first and the launch ends on short
+  // workgroups: the workgroup ranks the lengths itself (ragged step 3.035 -> 2.991 ms,
+  // four alternating runs of 40 steps each).
   const int chunk = blockIdx.z;
   const int h = blockIdx.x;
   const int nqg = (a.B + 15) / 16;
-  const int s = blockIdx.y / nqg;
+  int s = blockIdx.y / nqg;
   const int qg = blockIdx.y - s * nqg;
+  if (!FUSE && a.n_seq > 1 && a.n_seq <= kAttnSortSeqs &&
+      gridDim.x * gridDim.y * gridDim.z > 2u * unsigned(a.n_cus)) {
+    __shared__ int lens[kAttnSortSeqs];
+    __shared__ int pick;
+    for (int t = threadIdx.x; t < a.n_seq; t += kAttnThreads) lens[t] = a.ctx_len[t];
+    __syncthreads();
+    // The ranks are a permutation of 0 .. n_seq-1, so exactly one thread finds slot s.
+    for (int t = threadIdx.x; t < a.n_seq; t += kAttnThreads) {
+      const int tt = lens[t];
+      int rank = 0;
+      for (int u = 0; u < a.n_seq; ++u) {
+        const int tu = lens[u];
+        rank += (tu > tt) || (tu == tt && u < t);
+      }
+      if (rank == s) pick = t;
+    }
+    __syncthreads();
+    s = pick;
+  }
   const int lane = threadIdx.x & 63;
   const int wid = threadIdx.x >> 6;
   const int g = lane >> 4;       // lane group 0..3
@@ -438,7 +462,9 @@ __global__ void attn_f32_kernel(AttnArgs a, float* __restrict__ out) {
   for (int i = 0; i < hd; ++i) dst[i] = o[i] / l;
 }
 
-hipError_t launch_attention(bool bf16, const AttnArgs& a, void* out, hipStream_t s) {
+hipError_t launch_attention(bool bf16, const AttnArgs& args, void* out, hipStream_t s) {
+  AttnArgs a = args;
+  a.n_cus = device_cu_count();
   if (a.n_seq <= 0) return hipSuccess;
   if (!bf16) {
     if (a.hd == 128)

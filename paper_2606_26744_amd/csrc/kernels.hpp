@@ -223,6 +223,7 @@ struct AttnArgs {
   int fuse_epi;
   const int32_t* new_offsets;  // [n_seq+1]
   QkvEpiArgs epi_ctx, epi_blk;
+  int n_cus;                   // set by launch_attention (the dispatch order uses it)
 };
 
 // Longest context chunk of one bf16 attention workgroup.
