@@ -106,6 +106,18 @@ def test_many_sequences_attention_chunks():
     _compare(DraftCase(wl, ctx, [min(c, 16) for c in ctx], sub=13), seqs=[3, 5, 11])
 
 
+def test_longest_first_dispatch_every_sequence():
+    """40 sequences x 16 heads in 512-key chunks (1920 attention workgroups, more than two
+    rounds): each workgroup slot takes the sequence of its rank by context length, ties by
+    index.  Lengths with ties and an empty context; every sequence against the oracle."""
+    wl = synth.small_bf16()
+    rng = np.random.default_rng(41)
+    ctx = [int(x) for x in rng.integers(1, 600, size=40)]
+    ctx[3] = ctx[17] = ctx[29] = 333          # equal lengths: ranked by sequence index
+    ctx[8] = 0
+    _compare(DraftCase(wl, ctx, [min(c, 16) for c in ctx], sub=19))
+
+
 def test_many_sequences_attention_chunks_head_dim_128():
     wl = synth.small_bf16()
     wl.drafter = synth.DrafterShape(d=1024, n_layers=1, n_heads=8, head_dim=128, d_ff=2048,
