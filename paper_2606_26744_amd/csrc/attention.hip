@@ -82,7 +82,7 @@ attn_bf16_kernel(AttnArgs a, bf16_t* __restrict__ out) {
   int s = blockIdx.y / nqg;
   const int qg = blockIdx.y - s * nqg;
   if (!FUSE && a.n_seq > 1 && a.n_seq <= kAttnSortSeqs &&
-      gridDim.x * gridDim.y * gridDim.z > 2u * unsigned(a.n_cus)) {
+      uint64_t(gridDim.x) * gridDim.y * gridDim.z > 2ull * uint64_t(a.n_cus)) {
     __shared__ int lens[kAttnSortSeqs];
     __shared__ int pick;
     for (int t = threadIdx.x; t < a.n_seq; t += kAttnThreads) lens[t] = a.ctx_len[t];
