@@ -36,7 +36,11 @@ def test_warm_step_rows():
 
 
 @pytest.mark.parametrize("n,m,d,dtype,bias", [(37, 4, 256, "f32", True), (300, 3, 1024, "bf16", False),
-                                              (1, 8, 512, "bf16", True), (2050, 2, 128, "bf16", True)])
+                                              (1, 8, 512, "bf16", True), (2050, 2, 128, "bf16", True),
+                                              # more than 128 rows on the matrix-core tiles with
+                                              # K = 64 and 128: fewer 32-wide K units than the
+                                              # weight ring holds, and exactly as many
+                                              (257, 1, 64, "bf16", False), (300, 2, 64, "bf16", True)])
 def test_shapes(n, m, d, dtype, bias):
     _case(n, m, d, dtype, n + m, bias)
 
