@@ -15,6 +15,7 @@ on), the reducer at its bandwidth-stress size, and the CPU oracle timed on a bou
 sample on this host.
 """
 import argparse
+import gc
 import json
 import os
 import statistics
@@ -156,6 +157,7 @@ def ragged_leg(torch, synth, hdf, steps, warmup, wl=None, cpu_seqs=None):
         res["cpu_baseline"] = cpu_baseline(torch, synth, wl, h, w, red, args, offs, seqs=cpu_seqs,
                                            budget_s=10.0)
     del wl, h, bufs, args, red, w
+    gc.collect()
     torch.cuda.empty_cache()
     return res
 
@@ -266,6 +268,7 @@ def decode_leg(torch, synth, hdf, rounds, warmup):
                 "committed_tokens_per_s": round(committed / dt_sync, 1),
                 "mean_accept_len": round(committed / (rounds * n_seq) - 1, 3)}
     del dec
+    gc.collect()
     torch.cuda.empty_cache()
 
     # chained rounds
@@ -291,6 +294,7 @@ def decode_leg(torch, synth, hdf, rounds, warmup):
            "context_end": [int(x) for x in c1], "pages_used": n_pages - dec.pool.free,
            "host_synchronised": sync_res}
     del dec, h, w, red
+    gc.collect()
     torch.cuda.empty_cache()
     return res
 
@@ -326,6 +330,7 @@ def sampled_leg(torch, synth, hdf, wl, h, bufs, args, T, steps, warmup):
     res = {"temperature": T, "ms_per_step": round(ms, 4), "blocks_per_s": round(n_seq / (ms * 1e-3), 1),
            "steps": steps, "mean_accept_len": round(float(acc.mean()), 3)}
     del sb, tgt
+    gc.collect()
     torch.cuda.empty_cache()
     return res
 
@@ -355,6 +360,7 @@ def kl_leg(torch, synth, hdf, wl, h):
     res = {"n_seq": n, "B": B, "P": P, "vocab": V, "us": round(e0.elapsed_time(e1) / 10 * 1e3, 1),
            "loss": [round(float(x), 4) for x in out[2].cpu()]}
     del H, z, lab, ws
+    gc.collect()
     torch.cuda.empty_cache()
     return res
 
@@ -393,6 +399,7 @@ def fc_reducer_leg(torch, synth, hdf):
         row["fc_TFLOP/s"] = round(2.0 * n * m * d * d / (row["fc_us"] * 1e-6) / 1e12, 1)
         out.append(row)
         del ri, Wp, Y, ws
+        gc.collect()
         torch.cuda.empty_cache()
     return out
 
@@ -425,6 +432,7 @@ def blas_reference(torch):
         out.append({"gemm": name, "M": M, "K": K, "N": N, "us": round(us, 1),
                     "TFLOP/s": round(tf, 1), "mfma_frac": round(tf / BF16_PEAK_TFLOPS, 4)})
         del a, w, wt, c
+        gc.collect()
         torch.cuda.empty_cache()
     return out
 
@@ -656,6 +664,7 @@ def cold_cache_step(torch, h, bufs, args, tg, steps):
     torch.cuda.synchronize()
     ms = statistics.mean(a.elapsed_time(b) for a, b in ev)
     del src, dst
+    gc.collect()
     torch.cuda.empty_cache()
     return {"ms_per_step": round(ms, 4), "steps": steps,
             "flush": "512 MiB device copy before every step"}
@@ -701,6 +710,12 @@ def main():
     hdf.lib()
     wl, h, bufs, args, red, w, offs = build_workload(torch, synth, hdf)
     n_seq, B = wl.n_seq, wl.block
+    # Python's cyclic garbage collector stays paused from here on (collected now and where
+    # a leg frees its workload): a full pass over this process's heap takes tens of
+    # milliseconds, and a pass inside a timed loop leaves the GPU idle while the host is
+    # not enqueuing (a 20-step run once measured 4.0 ms a step for 0.38 ms of work).
+    gc.collect()
+    gc.disable()
     # Targets: copies of the drafts with probability 0.8 per position (drafts from one
     # untimed step), so acceptance lengths are geometric as in the workload description.
     tg = step_targets(torch, synth, hdf, wl, h, bufs, args)
@@ -796,6 +811,7 @@ def main():
         if not a.no_cpu_baseline:
             res["reducer_stress"]["cpu_baseline"] = cpu_reducer_baseline(synth, sw, ri)
         del ri, Y
+        gc.collect()
         torch.cuda.empty_cache()
     if a.copy_probe:
         x = torch.empty(1 << 31, dtype=torch.uint8, device="cuda")
@@ -820,6 +836,7 @@ def main():
                 e["frac_of_mfma_probe"] = round(e["TFLOP/s"] / res["mfma_probe"]["TFLOP/s"], 4)
     if not a.no_ragged or a.cold or a.ragged_cold or a.decode:
         del bufs, args
+        gc.collect()
         torch.cuda.empty_cache()
     if not a.no_ragged:
         res["ragged_decode"] = ragged_leg(torch, synth, hdf, max(a.steps // 5, 5), 3,
