@@ -118,6 +118,18 @@ def test_longest_first_dispatch_every_sequence():
     _compare(DraftCase(wl, ctx, [min(c, 16) for c in ctx], sub=19))
 
 
+def test_longest_first_dispatch_several_query_groups():
+    """The same ranking with B = 33: three 16-query groups per sequence slot (the last
+    holds one query), and every group's workgroup must take the slot's sequence.  Ties, an
+    empty context; every sequence against the oracle."""
+    wl = synth.small_bf16()
+    rng = np.random.default_rng(43)
+    ctx = [int(x) for x in rng.integers(1, 600, size=40)]
+    ctx[2] = ctx[21] = ctx[30] = 250
+    ctx[11] = 0
+    _compare(DraftCase(wl, ctx, [min(c, 33) for c in ctx], B=33, sub=20))
+
+
 def test_many_sequences_attention_chunks_head_dim_128():
     wl = synth.small_bf16()
     wl.drafter = synth.DrafterShape(d=1024, n_layers=1, n_heads=8, head_dim=128, d_ff=2048,
